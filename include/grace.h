@@ -1,0 +1,163 @@
+/*
+ * grace.h -- C ABI of the wide-beam decode attention library for MI355X (gfx950).
+ *
+ * One decode step of an encoder-decoder generative retriever under beam search
+ * (GRACE, arXiv 2608.00938):
+ *
+ *   grace_cross_attn      the beams of a request attend to that request's shared
+ *                         encoder K/V, beam-as-query layout (Sec. 5.1, App. B);
+ *   grace_kv_append       paged beam rearrangement: block-table rows copy their
+ *                         parent's ids, the current token takes a fresh block
+ *                         (Sec. 3.3, Sec. 5.3);
+ *   grace_self_attn_step  each beam attends over its short paged Semantic-ID
+ *                         prefix, positions 0..step (Sec. 5.2, Sec. 5.3).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory.  Pointers documented as "device" are HIP device allocations owned by
+ *   the caller.  The library allocates nothing, frees nothing and keeps no
+ *   pointer after it returns.
+ * Layout.  Row-major and contiguous.  Beam rows are request-major: row
+ *   r = b*M + m holds beam m of request b (App. B).  A token vector is [H, d]
+ *   (head-major), so a [rows, H, d] tensor has element (r, h, i) at
+ *   r*H*d + h*d + i.
+ * Types.  dtype is GRACE_F32 (float) or GRACE_BF16 (bfloat16) and applies to
+ *   every q/k/v/out/pool argument of the call.  Dot products, softmax and
+ *   accumulation run in fp32; outputs are rounded to nearest-even.
+ * Streams.  `stream` is a hipStream_t passed as void* (NULL = null stream).
+ *   Work is enqueued on it and not waited for; the library does no host
+ *   synchronisation and holds no global state besides the thread-local last
+ *   HIP error, so calls from several threads on several streams are safe.
+ * Errors.  Every argument check runs on the host before any launch; a
+ *   non-zero status means nothing was launched and nothing was written.  A
+ *   HIP launch failure returns GRACE_ERR_HIP and grace_last_hip_error() gives
+ *   the hipError_t code.  Supported: d in {32, 64, 128}; 1 <= T_max <= 8;
+ *   0 <= step < T_max; H >= 1; B, M >= 0 (B*M = 0 is a no-op); B*M*H*d and
+ *   T_max*B*M below 2^31.
+ */
+#ifndef GRACE_H
+#define GRACE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum grace_dtype { GRACE_F32 = 0, GRACE_BF16 = 1 };
+
+enum grace_status {
+  GRACE_OK = 0,
+  GRACE_ERR_NULL = 1,         /* a required pointer is NULL                     */
+  GRACE_ERR_SHAPE = 2,        /* a size or index argument is out of range       */
+  GRACE_ERR_UNSUPPORTED = 3,  /* dtype or head dim the library does not build   */
+  GRACE_ERR_ALIAS = 4,        /* an output overlaps an input it must not        */
+  GRACE_ERR_HIP = 5           /* a HIP runtime call failed; see grace_last_hip_error */
+};
+
+/*
+ * Cross-attention of every beam row against its request's encoder K/V, in the
+ * beam-as-query layout (Sec. 5.1; correctness of the layout: App. B).  For
+ * request b, head h and beam m:
+ *   out[b*M+m, h, :] = sum_j softmax_j(scale * <q[b*M+m, h, :], K[off[b]+j, h, :]>)
+ *                      * V[off[b]+j, h, :],   j = 0 .. L_b-1,  L_b = off[b+1]-off[b].
+ * The M beams of a request are the query rows of one contraction over K/V that
+ * the library reads once per beam tile; Q is read in its beam-major layout,
+ * with no permuted copy.
+ *
+ *   q        device, [B*M, H, d], dtype
+ *   enc_k    device, [sum_L, H, d], dtype; the requests' encoder keys packed
+ *            without padding, request b at rows off[b] .. off[b+1]-1
+ *   enc_v    device, [sum_L, H, d], dtype; values, same packing
+ *   enc_off  device, int32 [B+1]; enc_off[0] = 0, non-decreasing,
+ *            enc_off[B] = sum_L.  Entries are clamped to [0, sum_L] on the
+ *            device, so a bad table cannot read out of bounds (its rows are
+ *            then unspecified).  A request with L_b = 0 gets zero output rows.
+ *   B, M     requests and beams per request
+ *   H, d     heads and head dim (d in {32, 64, 128})
+ *   sum_L    total encoder tokens (rows of enc_k / enc_v); >= 0
+ *   scale    softmax scale, finite and > 0 (1/sqrt(d) for standard attention)
+ *   dtype    GRACE_F32 or GRACE_BF16
+ *   out      device, [B*M, H, d], dtype; must not overlap q, enc_k or enc_v
+ *   stream   hipStream_t
+ */
+int32_t grace_cross_attn(const void* q, const void* enc_k, const void* enc_v,
+                         const int32_t* enc_off, int32_t B, int32_t M, int32_t H, int32_t d,
+                         int32_t sum_L, float scale, int32_t dtype, void* out, void* stream);
+
+/*
+ * Paged beam rearrangement and append of the current token at decode step
+ * `step` (Sec. 3.3, Sec. 5.3).  The KV pool stores one block per generated
+ * token of one beam row, across all heads; block id t*R + r (R = B*M) is slab t,
+ * row r of a pool laid out [T_max, R, H, d].  For every row i = b*M + m:
+ *   table_next[i, j]    = table_prev[b*M + parents[i], j]   for 0 <= j < step
+ *   table_next[i, step] = step*R + i                        (its fresh block)
+ *   k_pool[step, i, :, :] = k_new[i],  v_pool[step, i, :, :] = v_new[i]
+ * Only block ids move for the prefix; no cached K/V bytes are copied.
+ * Columns j > step of table_next are not written.
+ *
+ *   k_pool, v_pool  device, [T_max, B*M, H, d], dtype
+ *   table_prev      device, int32 [B*M, T_max]; read for step > 0 (NULL allowed at step 0)
+ *   table_next      device, int32 [B*M, T_max]; written; must not overlap table_prev
+ *   parents         device, int32 [B*M]; request-local parent beam in [0, M) of each
+ *                   new row (NULL allowed at step 0, where parents are ignored).
+ *                   An entry outside [0, M) is clamped into range and sets *err_flag.
+ *   k_new, v_new    device, [B*M, H, d], dtype; the current token's key and value.
+ *                   A pointer equal to its pool's slab `step` is taken as already
+ *                   in place and that copy is skipped; any other overlap with the
+ *                   written slab is GRACE_ERR_ALIAS.
+ *   B, M, H, d      as for grace_cross_attn
+ *   T_max           pool slabs and table columns (1 .. 8)
+ *   step            decode step, 0 <= step < T_max
+ *   dtype           GRACE_F32 or GRACE_BF16
+ *   err_flag        device int32 or NULL; set to 1 when a parent was out of range,
+ *                   never cleared by the library
+ *   stream          hipStream_t
+ */
+int32_t grace_kv_append(void* k_pool, void* v_pool, const int32_t* table_prev,
+                        int32_t* table_next, const int32_t* parents, const void* k_new,
+                        const void* v_new, int32_t B, int32_t M, int32_t H, int32_t d,
+                        int32_t T_max, int32_t step, int32_t dtype, int32_t* err_flag,
+                        void* stream);
+
+/*
+ * Self-attention at decode step `step` over each beam's paged prefix
+ * (Sec. 5.2, Sec. 5.3).  Row r gathers the step+1 blocks table[r, 0..step] in
+ * prefix order; there is no other mask.  For every row r and head h:
+ *   out[r, h, :] = sum_j softmax_j(scale * <q[r, h, :], Kblk(table[r, j])[h, :]>)
+ *                  * Vblk(table[r, j])[h, :],   j = 0 .. step
+ * where Kblk(id) is k_pool viewed as [T_max*B*M, H, d].  Block ids are clamped
+ * into [0, T_max*B*M) on the device, so an unwritten table entry cannot read
+ * out of bounds (that row's output is then unspecified).
+ *
+ *   q               device, [B*M, H, d], dtype
+ *   k_pool, v_pool  device, [T_max, B*M, H, d], dtype
+ *   table           device, int32 [B*M, T_max]; columns 0..step are read
+ *   B, M, H, d      as for grace_cross_attn
+ *   T_max, step     as for grace_kv_append
+ *   scale           softmax scale, finite and > 0
+ *   dtype           GRACE_F32 or GRACE_BF16
+ *   out             device, [B*M, H, d], dtype; must not overlap q or the pools
+ *   stream          hipStream_t
+ */
+int32_t grace_self_attn_step(const void* q, const void* k_pool, const void* v_pool,
+                             const int32_t* table, int32_t B, int32_t M, int32_t H, int32_t d,
+                             int32_t T_max, int32_t step, float scale, int32_t dtype, void* out,
+                             void* stream);
+
+/* Human-readable name of a status code (static storage; never NULL). */
+const char* grace_status_string(int32_t status);
+
+/* hipError_t of the last failed HIP call in this thread (0 if none). */
+int32_t grace_last_hip_error(void);
+
+/* ABI version of this header; bumped on any incompatible change. */
+int32_t grace_abi_version(void);
+
+#define GRACE_ABI_VERSION 1
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GRACE_H */

@@ -1,0 +1,140 @@
+// C ABI of the decode-attention library: argument validation on the host,
+// dispatch to the gfx950 kernels, HIP error mapping.  Nothing here allocates,
+// synchronises or keeps state beyond the thread-local last HIP error.
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/grace.h"
+#include "kernels.hpp"
+
+namespace {
+
+thread_local int32_t g_last_hip_error = 0;
+
+bool supported_d(int32_t d) { return d == 32 || d == 64 || d == 128; }
+
+int32_t elem_bytes(int32_t dtype) { return dtype == GRACE_F32 ? 4 : 2; }
+
+// Byte ranges [a, a+na) and [b, b+nb) overlap.
+bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
+  if (na <= 0 || nb <= 0) return false;
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
+}
+
+int32_t hip_status(hipError_t e) {
+  if (e == hipSuccess) return GRACE_OK;
+  g_last_hip_error = (int32_t)e;
+  return GRACE_ERR_HIP;
+}
+
+// Common shape checks; sets rows and row bytes.
+int32_t check_shape(int32_t B, int32_t M, int32_t H, int32_t d, int32_t dtype, int64_t& R,
+                    int64_t& row_bytes) {
+  if (dtype != GRACE_F32 && dtype != GRACE_BF16) return GRACE_ERR_UNSUPPORTED;
+  if (!supported_d(d)) return GRACE_ERR_UNSUPPORTED;
+  if (B < 0 || M < 0 || H < 1) return GRACE_ERR_SHAPE;
+  R = (int64_t)B * M;
+  if (R * H * d >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
+  row_bytes = (int64_t)H * d * elem_bytes(dtype);
+  return GRACE_OK;
+}
+
+bool good_scale(float scale) { return isfinite(scale) && scale > 0.f; }
+
+}  // namespace
+
+extern "C" {
+
+int32_t grace_abi_version(void) { return GRACE_ABI_VERSION; }
+
+int32_t grace_last_hip_error(void) { return g_last_hip_error; }
+
+const char* grace_status_string(int32_t status) {
+  switch (status) {
+    case GRACE_OK: return "ok";
+    case GRACE_ERR_NULL: return "required pointer is NULL";
+    case GRACE_ERR_SHAPE: return "size or index argument out of range";
+    case GRACE_ERR_UNSUPPORTED: return "unsupported dtype or head dim";
+    case GRACE_ERR_ALIAS: return "output overlaps an input";
+    case GRACE_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int32_t grace_cross_attn(const void* q, const void* enc_k, const void* enc_v,
+                         const int32_t* enc_off, int32_t B, int32_t M, int32_t H, int32_t d,
+                         int32_t sum_L, float scale, int32_t dtype, void* out, void* stream) {
+  int64_t R, row_bytes;
+  int32_t st = check_shape(B, M, H, d, dtype, R, row_bytes);
+  if (st != GRACE_OK) return st;
+  if (sum_L < 0 || (int64_t)sum_L * H * d >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
+  if (!good_scale(scale)) return GRACE_ERR_SHAPE;
+  if (R == 0) return GRACE_OK;
+  if (!q || !out || !enc_off || (sum_L > 0 && (!enc_k || !enc_v))) return GRACE_ERR_NULL;
+  const int64_t qo_bytes = R * row_bytes, kv_bytes = (int64_t)sum_L * row_bytes;
+  if (overlaps(out, qo_bytes, q, qo_bytes) || overlaps(out, qo_bytes, enc_k, kv_bytes) ||
+      overlaps(out, qo_bytes, enc_v, kv_bytes) || overlaps(out, qo_bytes, enc_off, 4 * (B + 1)))
+    return GRACE_ERR_ALIAS;
+  return hip_status(grace::launch_cross_attn(q, enc_k, enc_v, enc_off, out, B, M, H, d, sum_L,
+                                             scale, dtype == GRACE_BF16, (hipStream_t)stream));
+}
+
+int32_t grace_kv_append(void* k_pool, void* v_pool, const int32_t* table_prev,
+                        int32_t* table_next, const int32_t* parents, const void* k_new,
+                        const void* v_new, int32_t B, int32_t M, int32_t H, int32_t d,
+                        int32_t T_max, int32_t step, int32_t dtype, int32_t* err_flag,
+                        void* stream) {
+  int64_t R, row_bytes;
+  int32_t st = check_shape(B, M, H, d, dtype, R, row_bytes);
+  if (st != GRACE_OK) return st;
+  if (T_max < 1 || T_max > 8 || step < 0 || step >= T_max) return GRACE_ERR_SHAPE;
+  if ((int64_t)T_max * R >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
+  if (R == 0) return GRACE_OK;
+  if (!k_pool || !v_pool || !table_next || !k_new || !v_new) return GRACE_ERR_NULL;
+  if (step > 0 && (!table_prev || !parents)) return GRACE_ERR_NULL;
+  const int64_t slab = R * row_bytes, table_bytes = R * T_max * 4;
+  char* k_slab = (char*)k_pool + step * slab;
+  char* v_slab = (char*)v_pool + step * slab;
+  if (step > 0 && overlaps(table_next, table_bytes, table_prev, table_bytes)) return GRACE_ERR_ALIAS;
+  if (step > 0 && overlaps(table_next, table_bytes, parents, R * 4)) return GRACE_ERR_ALIAS;
+  if (overlaps(k_slab, slab, v_slab, slab)) return GRACE_ERR_ALIAS;
+  const bool copy_k = k_new != (const void*)k_slab;
+  const bool copy_v = v_new != (const void*)v_slab;
+  // A source that is not exactly its slab must not overlap any written slab.
+  if (copy_k && (overlaps(k_new, slab, k_slab, slab) || overlaps(k_new, slab, v_slab, slab)))
+    return GRACE_ERR_ALIAS;
+  if (copy_v && (overlaps(v_new, slab, v_slab, slab) || overlaps(v_new, slab, k_slab, slab)))
+    return GRACE_ERR_ALIAS;
+  const int64_t pool_bytes = slab * T_max;
+  if (overlaps(table_next, table_bytes, k_pool, pool_bytes) ||
+      overlaps(table_next, table_bytes, v_pool, pool_bytes))
+    return GRACE_ERR_ALIAS;
+  return hip_status(grace::launch_kv_append(k_slab, v_slab, table_prev, table_next, parents,
+                                            k_new, v_new, (int32_t)R, M, T_max, step,
+                                            (int32_t)row_bytes, copy_k, copy_v, err_flag,
+                                            (hipStream_t)stream));
+}
+
+int32_t grace_self_attn_step(const void* q, const void* k_pool, const void* v_pool,
+                             const int32_t* table, int32_t B, int32_t M, int32_t H, int32_t d,
+                             int32_t T_max, int32_t step, float scale, int32_t dtype, void* out,
+                             void* stream) {
+  int64_t R, row_bytes;
+  int32_t st = check_shape(B, M, H, d, dtype, R, row_bytes);
+  if (st != GRACE_OK) return st;
+  if (T_max < 1 || T_max > 8 || step < 0 || step >= T_max) return GRACE_ERR_SHAPE;
+  if ((int64_t)T_max * R >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
+  if (!good_scale(scale)) return GRACE_ERR_SHAPE;
+  if (R == 0) return GRACE_OK;
+  if (!q || !k_pool || !v_pool || !table || !out) return GRACE_ERR_NULL;
+  const int64_t slab = R * row_bytes, pool_bytes = slab * T_max;
+  if (overlaps(out, slab, q, slab) || overlaps(out, slab, k_pool, pool_bytes) ||
+      overlaps(out, slab, v_pool, pool_bytes) || overlaps(out, slab, table, R * T_max * 4))
+    return GRACE_ERR_ALIAS;
+  return hip_status(grace::launch_self_attn_step(q, k_pool, v_pool, table, out, (int32_t)R, H, d,
+                                                 T_max, step, scale, dtype == GRACE_BF16,
+                                                 (hipStream_t)stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,28 @@
+// Internal launchers of the gfx950 kernels; the C ABI in grace_api.hip calls
+// them after validating every argument.  Each returns the launch's HIP status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace grace {
+
+// Cross-attention, beam-as-query: grid over (request, head, beam tile).
+hipError_t launch_cross_attn(const void* q, const void* enc_k, const void* enc_v,
+                             const int32_t* enc_off, void* out, int32_t B, int32_t M, int32_t H,
+                             int32_t d, int32_t sum_L, float scale, bool bf16, hipStream_t stream);
+
+// Paged rearrangement + append.  k_slab/v_slab point at slab `step` of the pools.
+hipError_t launch_kv_append(void* k_slab, void* v_slab, const int32_t* table_prev,
+                            int32_t* table_next, const int32_t* parents, const void* k_new,
+                            const void* v_new, int32_t R, int32_t M, int32_t T_max, int32_t step,
+                            int32_t row_bytes, bool copy_k, bool copy_v, int32_t* err_flag,
+                            hipStream_t stream);
+
+// Paged self-attention over step+1 tokens.
+hipError_t launch_self_attn_step(const void* q, const void* k_pool, const void* v_pool,
+                                 const int32_t* table, void* out, int32_t R, int32_t H, int32_t d,
+                                 int32_t T_max, int32_t step, float scale, bool bf16,
+                                 hipStream_t stream);
+
+}  // namespace grace

@@ -1,0 +1,163 @@
+"""Python binding of libgrace.so (argument marshalling only).
+
+The three entry points keep their C names and take torch tensors that already
+live on the GPU; each call passes raw device pointers, sizes, the dtype code and
+the current HIP stream to the library and turns a non-zero status into
+:class:`GraceError`.  Every step of the computation runs in the library's HIP
+kernels; there is no other code path, and a missing build raises on first use.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgrace.so")
+_lib = None
+
+GRACE_F32, GRACE_BF16 = 0, 1
+GRACE_OK, GRACE_ERR_NULL, GRACE_ERR_SHAPE, GRACE_ERR_UNSUPPORTED, GRACE_ERR_ALIAS, GRACE_ERR_HIP = range(6)
+
+_DTYPE_CODE = {torch.float32: GRACE_F32, torch.bfloat16: GRACE_BF16}
+
+_c_int, _c_float, _c_void_p = ctypes.c_int32, ctypes.c_float, ctypes.c_void_p
+_SIGNATURES = {
+    "grace_cross_attn": [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_int, _c_int, _c_int,
+                         _c_int, _c_int, _c_float, _c_int, _c_void_p, _c_void_p],
+    "grace_kv_append": [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+                        _c_void_p, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
+                        _c_void_p, _c_void_p],
+    "grace_self_attn_step": [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_int, _c_int, _c_int,
+                             _c_int, _c_int, _c_int, _c_float, _c_int, _c_void_p, _c_void_p],
+    "grace_status_string": [_c_int],
+    "grace_last_hip_error": [],
+    "grace_abi_version": [],
+}
+
+
+class GraceError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        msg = library().grace_status_string(status).decode()
+        if status == GRACE_ERR_HIP:
+            msg += f" (hipError {library().grace_last_hip_error()})"
+        super().__init__(f"{where}: {msg} [status {status}]")
+
+
+def library() -> ctypes.CDLL:
+    """The loaded libgrace.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is missing: build it with "
+                               "`python -m paper_2608_00938_amd.build`")
+        lib = ctypes.CDLL(_LIB_PATH)
+        for name, args in _SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.argtypes = args
+            fn.restype = ctypes.c_char_p if name == "grace_status_string" else _c_int
+        _lib = lib
+    return _lib
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(t: torch.Tensor):
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _check(status: int, where: str):
+    if status != GRACE_OK:
+        raise GraceError(status, where)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    try:
+        return _DTYPE_CODE[t.dtype]
+    except KeyError:
+        raise TypeError(f"unsupported dtype {t.dtype}") from None
+
+
+def _contig(*ts):
+    for t in ts:
+        if t is not None and not t.is_contiguous():
+            raise ValueError("tensors passed to libgrace must be contiguous")
+
+
+def grace_cross_attn(q, enc_k, enc_v, enc_off, M: int, scale: float | None = None, out=None):
+    """Beam-as-query cross-attention; q [B*M, H, d], enc_k/enc_v [sum_L, H, d],
+    enc_off int32 [B+1] on the device.  Returns out [B*M, H, d]."""
+    _contig(q, enc_k, enc_v, enc_off, out)
+    R, H, d = q.shape
+    B = enc_off.numel() - 1
+    if M <= 0 and R == 0:
+        M = 0
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    if out is None:
+        out = torch.empty_like(q)
+    st = library().grace_cross_attn(_ptr(q), _ptr(enc_k), _ptr(enc_v), _ptr(enc_off), B, M, H, d,
+                                    enc_k.shape[0], scale, _dtype_code(q), _ptr(out), _stream(q))
+    _check(st, "grace_cross_attn")
+    return out
+
+
+def grace_kv_append(k_pool, v_pool, table_prev, table_next, parents, k_new, v_new, B: int,
+                    M: int, step: int, err_flag=None):
+    """Paged rearrangement + append at ``step``; pools [T_max, B*M, H, d], tables
+    int32 [B*M, T_max], parents int32 [B*M] (None at step 0)."""
+    _contig(k_pool, v_pool, table_prev, table_next, parents, k_new, v_new)
+    T_max, R, H, d = k_pool.shape
+    st = library().grace_kv_append(_ptr(k_pool), _ptr(v_pool), _ptr(table_prev), _ptr(table_next),
+                                   _ptr(parents), _ptr(k_new), _ptr(v_new), B, M, H, d, T_max,
+                                   step, _dtype_code(k_pool), _ptr(err_flag), _stream(k_pool))
+    _check(st, "grace_kv_append")
+
+
+def grace_self_attn_step(q, k_pool, v_pool, table, B: int, M: int, step: int,
+                         scale: float | None = None, out=None):
+    """Paged self-attention over step+1 tokens; returns out [B*M, H, d]."""
+    _contig(q, k_pool, v_pool, table, out)
+    T_max, R, H, d = k_pool.shape
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    if out is None:
+        out = torch.empty_like(q)
+    st = library().grace_self_attn_step(_ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(table), B, M,
+                                        H, d, T_max, step, scale, _dtype_code(q), _ptr(out),
+                                        _stream(q))
+    _check(st, "grace_self_attn_step")
+    return out
+
+
+class KVCache:
+    """Caller-side storage of the paged self-attention cache: the two pools and
+    a pair of block tables used alternately (the update reads one, writes the
+    other).  Allocation is torch's; all work is the library's."""
+
+    def __init__(self, B: int, M: int, H: int, d: int, T_max: int, dtype: torch.dtype,
+                 device="cuda"):
+        self.B, self.M, self.H, self.d, self.T_max = B, M, H, d, T_max
+        R = B * M
+        self.k_pool = torch.empty((T_max, R, H, d), dtype=dtype, device=device)
+        self.v_pool = torch.empty((T_max, R, H, d), dtype=dtype, device=device)
+        self.tables = [torch.zeros((R, T_max), dtype=torch.int32, device=device) for _ in range(2)]
+        self.err_flag = torch.zeros(1, dtype=torch.int32, device=device)
+
+    def table(self, step: int) -> torch.Tensor:
+        """Block table valid after the append of ``step``."""
+        return self.tables[step % 2]
+
+    def slab(self, step: int):
+        """Views of pool slab ``step``: writing k_new/v_new here makes the append copy-free."""
+        return self.k_pool[step], self.v_pool[step]
+
+    def append(self, step: int, k_new, v_new, parents=None):
+        grace_kv_append(self.k_pool, self.v_pool, self.tables[(step + 1) % 2], self.tables[step % 2],
+                        parents, k_new, v_new, self.B, self.M, step, self.err_flag)
+
+    def attend(self, step: int, q, scale: float | None = None, out=None):
+        return grace_self_attn_step(q, self.k_pool, self.v_pool, self.table(step), self.B, self.M,
+                                    step, scale=scale, out=out)

@@ -1,0 +1,121 @@
+"""The C ABI on the host: the library loads, exports every symbol the header
+declares, and rejects bad arguments before any launch (no GPU needed: every
+call here returns from the host-side checks)."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+from paper_2608_00938_amd import grace as G
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "grace.h")
+
+lib_missing = not os.path.exists(G._LIB_PATH)
+pytestmark = pytest.mark.skipif(lib_missing, reason="libgrace.so not built")
+
+P = ctypes.c_void_p(0x10000)    # never dereferenced: every call below fails a host check
+P2 = ctypes.c_void_p(0x20000)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(grace_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("grace_cross_attn", "grace_kv_append", "grace_self_attn_step"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = G.library()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    assert lib.grace_abi_version() == 1
+    assert lib.grace_last_hip_error() == 0
+    for st in range(6):
+        assert lib.grace_status_string(st)
+
+
+def cross(**kw):
+    a = dict(q=P, k=P2, v=P2, off=P2, B=2, M=4, H=2, d=64, sum_L=8, scale=0.125, dtype=1, out=P,
+             stream=None)
+    a.update(kw)
+    return G.library().grace_cross_attn(a["q"], a["k"], a["v"], a["off"], a["B"], a["M"], a["H"],
+                                        a["d"], a["sum_L"], a["scale"], a["dtype"], a["out"],
+                                        a["stream"])
+
+
+def append(**kw):
+    a = dict(kp=ctypes.c_void_p(0x100000), vp=ctypes.c_void_p(0x200000), tp=ctypes.c_void_p(0x300000),
+             tn=ctypes.c_void_p(0x400000), par=ctypes.c_void_p(0x500000), kn=ctypes.c_void_p(0x600000),
+             vn=ctypes.c_void_p(0x700000), B=2, M=4, H=2, d=64, T=4, step=1, dtype=1, err=None, stream=None)
+    a.update(kw)
+    return G.library().grace_kv_append(a["kp"], a["vp"], a["tp"], a["tn"], a["par"], a["kn"], a["vn"],
+                                       a["B"], a["M"], a["H"], a["d"], a["T"], a["step"], a["dtype"],
+                                       a["err"], a["stream"])
+
+
+def selfattn(**kw):
+    a = dict(q=ctypes.c_void_p(0x100000), kp=ctypes.c_void_p(0x200000), vp=ctypes.c_void_p(0x300000),
+             tab=ctypes.c_void_p(0x400000), B=2, M=4, H=2, d=64, T=4, step=1, scale=0.125, dtype=1,
+             out=ctypes.c_void_p(0x500000), stream=None)
+    a.update(kw)
+    return G.library().grace_self_attn_step(a["q"], a["kp"], a["vp"], a["tab"], a["B"], a["M"], a["H"],
+                                            a["d"], a["T"], a["step"], a["scale"], a["dtype"], a["out"],
+                                            a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(d=48), G.GRACE_ERR_UNSUPPORTED), (dict(d=256), G.GRACE_ERR_UNSUPPORTED),
+    (dict(dtype=7), G.GRACE_ERR_UNSUPPORTED), (dict(H=0), G.GRACE_ERR_SHAPE),
+    (dict(B=-1), G.GRACE_ERR_SHAPE), (dict(M=-3), G.GRACE_ERR_SHAPE),
+    (dict(sum_L=-1), G.GRACE_ERR_SHAPE), (dict(scale=0.0), G.GRACE_ERR_SHAPE),
+    (dict(scale=-1.0), G.GRACE_ERR_SHAPE), (dict(scale=math.nan), G.GRACE_ERR_SHAPE),
+    (dict(scale=math.inf), G.GRACE_ERR_SHAPE), (dict(q=None), G.GRACE_ERR_NULL),
+    (dict(out=None), G.GRACE_ERR_NULL), (dict(off=None), G.GRACE_ERR_NULL),
+    (dict(k=None), G.GRACE_ERR_NULL), (dict(out=P2), G.GRACE_ERR_ALIAS),
+    (dict(B=1 << 20, M=1 << 12, H=16), G.GRACE_ERR_SHAPE),
+    (dict(B=0), G.GRACE_OK), (dict(M=0, q=None, out=None), G.GRACE_OK),
+])
+def test_cross_attn_rejects(kw, status):
+    assert cross(**kw) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(T=0), G.GRACE_ERR_SHAPE), (dict(T=9), G.GRACE_ERR_SHAPE),
+    (dict(step=4), G.GRACE_ERR_SHAPE), (dict(step=-1), G.GRACE_ERR_SHAPE),
+    (dict(d=16), G.GRACE_ERR_UNSUPPORTED), (dict(dtype=2), G.GRACE_ERR_UNSUPPORTED),
+    (dict(kp=None), G.GRACE_ERR_NULL), (dict(tn=None), G.GRACE_ERR_NULL),
+    (dict(tp=None), G.GRACE_ERR_NULL), (dict(par=None), G.GRACE_ERR_NULL),
+    (dict(tn=ctypes.c_void_p(0x300000)), G.GRACE_ERR_ALIAS),       # table_next == table_prev
+    (dict(tn=ctypes.c_void_p(0x300010)), G.GRACE_ERR_ALIAS),       # partial overlap
+    (dict(kn=ctypes.c_void_p(0x100000 + 8 * 256 + 64)), G.GRACE_ERR_ALIAS),  # inside slab 1
+    (dict(B=0), G.GRACE_OK),
+])
+def test_kv_append_rejects(kw, status):
+    assert append(**kw) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(T=9), G.GRACE_ERR_SHAPE), (dict(step=4), G.GRACE_ERR_SHAPE),
+    (dict(scale=0.0), G.GRACE_ERR_SHAPE), (dict(d=100), G.GRACE_ERR_UNSUPPORTED),
+    (dict(tab=None), G.GRACE_ERR_NULL),
+    (dict(out=ctypes.c_void_p(0x100000)), G.GRACE_ERR_ALIAS),
+    (dict(out=ctypes.c_void_p(0x200000 + 100)), G.GRACE_ERR_ALIAS),
+    (dict(M=0), G.GRACE_OK),
+])
+def test_self_attn_rejects(kw, status):
+    assert selfattn(**kw) == status
+
+
+def test_binding_raises_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(G, "_lib", None)
+    monkeypatch.setattr(G, "_LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        G.library()

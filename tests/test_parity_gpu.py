@@ -1,0 +1,289 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle on the GPU.
+
+Small workloads are compared element by element on every output; the two
+largest are compared on sampled rows the oracle computes one request / one
+ancestor chain at a time, in exactly the launch configuration the benchmark
+times.  Tolerances: max abs error <= 2e-2 for bf16 inputs (fp32 accumulation),
+<= 1e-5 for fp32.  Integer work (block tables) and the pool copy are bit-exact.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_00938_amd import grace as G
+from paper_2608_00938_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"bf16": 2e-2, "f32": 1e-5}
+
+
+def _log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _np(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+class Decode:
+    """Runs the full decode of a workload on the GPU, one call per entry point per step."""
+
+    def __init__(self, wl, seed, device, keep_inputs=True):
+        self.wl, self.seed = wl, seed
+        self.inp = W.DecodeInputs(wl, seed, device)
+        self.enc_k, self.enc_v = self.inp.enc_kv
+        self.off = self.inp.offsets_tensor()
+        self.scale = 1.0 / math.sqrt(wl.d)
+        self.cache = G.KVCache(wl.B, wl.M, wl.H, wl.d, wl.steps, wl.torch_dtype, device)
+        self.parents = [self.inp.parents(t) for t in range(wl.steps)]
+        self.steps = []
+
+    def run_step(self, t):
+        wl, inp = self.wl, self.inp
+        qc = inp.step_tensor("q_cross", t)
+        qs = inp.step_tensor("q_self", t)
+        kn = inp.step_tensor("k_new", t)
+        vn = inp.step_tensor("v_new", t)
+        par = None if self.parents[t] is None else torch.from_numpy(self.parents[t]).to(qc.device)
+        xc = G.grace_cross_attn(qc, self.enc_k, self.enc_v, self.off, wl.M, self.scale)
+        self.cache.append(t, kn, vn, par)
+        xs = self.cache.attend(t, qs, self.scale)
+        rec = dict(qc=qc, qs=qs, kn=kn, vn=vn, xc=xc, xs=xs,
+                   table=self.cache.table(t).clone())
+        self.steps.append(rec)
+        return rec
+
+
+def _check_close(got, ref, dtype, what):
+    err = float(np.max(np.abs(got - ref))) if got.size else 0.0
+    _log(f"  {what}: max|err| = {err:.3e}  max|out| = {float(np.max(np.abs(ref))) if ref.size else 0:.3f}")
+    assert np.all(np.isfinite(got)), what
+    assert err <= TOL[dtype], f"{what}: {err} > {TOL[dtype]}"
+
+
+def _full_check(dec):
+    """Every output of every step against the oracle."""
+    wl = dec.wl
+    ek, ev = _np(dec.enc_k), _np(dec.enc_v)
+    kp = np.zeros((wl.steps, wl.R, wl.H, wl.d))
+    vp = np.zeros_like(kp)
+    table = np.zeros((wl.R, wl.steps), dtype=np.int64)
+    for t, rec in enumerate(dec.steps):
+        ref = oracle.cross_attn(_np(rec["qc"]), ek, ev, dec.inp.offsets, wl.M, dec.scale)
+        _check_close(_np(rec["xc"]), ref, wl.dtype, f"cross t={t}")
+        kp, vp, tnew = oracle.kv_append(kp, vp, table, dec.parents[t], _np(rec["kn"]),
+                                        _np(rec["vn"]), wl.B, wl.M, t)
+        table = np.zeros((wl.R, wl.steps), dtype=np.int64)
+        table[:, :t + 1] = tnew
+        gpu_table = rec["table"].cpu().numpy()[:, :t + 1]
+        assert np.array_equal(gpu_table, tnew), f"table t={t}"
+        ref = oracle.self_attn_step(_np(rec["qs"]), kp, vp, table, t, dec.scale)
+        _check_close(_np(rec["xs"]), ref, wl.dtype, f"self t={t}")
+    # the pool holds every step's token bit-exactly
+    for t, rec in enumerate(dec.steps):
+        assert torch.equal(dec.cache.k_pool[t], rec["kn"]) and torch.equal(dec.cache.v_pool[t], rec["vn"])
+
+
+def _sample_rows(wl, rng, n=48):
+    R, M = wl.R, wl.M
+    reqs = sorted({0, wl.B - 1, wl.B // 2, *rng.integers(0, wl.B, size=3).tolist()})
+    rows = []
+    for b in reqs:
+        beams = {0, 1, 31, 32, 63, 64, 255, 256, M - 1, *rng.integers(0, M, size=n // len(reqs)).tolist()}
+        rows += [b * M + m for m in sorted(x for x in beams if 0 <= x < M)]
+    return np.array(sorted(set(rows)), dtype=np.int64)
+
+
+def _sampled_check(dec, rng):
+    """Sampled rows, each computed by the oracle from its request / ancestor chain."""
+    wl = dec.wl
+    rows = _sample_rows(wl, rng)
+    dev = dec.enc_k.device
+    idx = torch.from_numpy(rows).to(dev)
+    for t, rec in enumerate(dec.steps):
+        # cross-attention: one request at a time
+        got = _np(rec["xc"].index_select(0, idx))
+        ref = np.empty_like(got)
+        for b in np.unique(rows // wl.M):
+            sel = np.nonzero(rows // wl.M == b)[0]
+            o0, o1 = int(dec.inp.offsets[b]), int(dec.inp.offsets[b + 1])
+            ref[sel] = oracle.cross_attn_request(_np(rec["qc"].index_select(0, idx[sel])),
+                                                 _np(dec.enc_k[o0:o1]), _np(dec.enc_v[o0:o1]),
+                                                 dec.scale)
+        _check_close(got, ref, wl.dtype, f"cross t={t} ({len(rows)} sampled rows)")
+        # block table rows from the parents alone, bit-exact
+        tab = oracle.table_rows(rows, t, dec.parents, wl.B, wl.M)
+        gpu_tab = rec["table"].index_select(0, idx).cpu().numpy()[:, :t + 1]
+        assert np.array_equal(gpu_tab, tab), f"table t={t}"
+        # self-attention: gather each sampled row's prefix from the step inputs
+        kpre = np.empty((len(rows), t + 1, wl.H, wl.d))
+        vpre = np.empty_like(kpre)
+        for j in range(t + 1):
+            src = torch.from_numpy(tab[:, j] - j * wl.R).to(dev)
+            kpre[:, j] = _np(dec.steps[j]["kn"].index_select(0, src))
+            vpre[:, j] = _np(dec.steps[j]["vn"].index_select(0, src))
+        ref = oracle.self_attn_rows(_np(rec["qs"].index_select(0, idx)), kpre, vpre, dec.scale)
+        _check_close(_np(rec["xs"].index_select(0, idx)), ref, wl.dtype,
+                     f"self t={t} ({len(rows)} sampled rows)")
+        assert torch.equal(dec.cache.k_pool[t], rec["kn"]) and torch.equal(dec.cache.v_pool[t], rec["vn"])
+
+
+@pytest.mark.parametrize("name", ["tiny_fp32", "bf16_b8_m256", "bf16_b32_m1024"])
+def test_workload_full_parity(gpu, name):
+    wl = W.WORKLOADS[name]
+    _log(f"[parity full] {name} seed=0")
+    dec = Decode(wl, 0, gpu)
+    for t in range(wl.steps):
+        dec.run_step(t)
+    torch.cuda.synchronize()
+    _full_check(dec)
+
+
+@pytest.mark.parametrize("name", ["bf16_b64_m4096", "bf16_ragged_b128_m2048"])
+def test_workload_sampled_parity(gpu, name):
+    wl = W.WORKLOADS[name]
+    _log(f"[parity sampled] {name} seed=0")
+    dec = Decode(wl, 0, gpu)
+    for t in range(wl.steps):
+        dec.run_step(t)
+    torch.cuda.synchronize()
+    assert int(dec.cache.err_flag.item()) == 0
+    _sampled_check(dec, np.random.default_rng(0))
+    # properties at full size: finite everywhere; t=0 self-attention is v_new
+    for rec in dec.steps:
+        assert bool(torch.isfinite(rec["xc"]).all()) and bool(torch.isfinite(rec["xs"]).all())
+    assert torch.equal(dec.steps[0]["xs"], dec.steps[0]["vn"])
+
+
+EDGE = [
+    # ragged tails: beams not a multiple of the 256-beam tile, keys not of the 64-token tile
+    dict(dtype="bf16", B=3, M=300, H=3, d=64, steps=3, L_lo=1, L_hi=130),
+    dict(dtype="bf16", B=2, M=17, H=1, d=32, steps=4, L_lo=60, L_hi=70),
+    dict(dtype="bf16", B=2, M=513, H=2, d=128, steps=5, L_lo=63, L_hi=200),
+    dict(dtype="f32", B=3, M=70, H=2, d=64, steps=3, L_lo=1, L_hi=100),
+    dict(dtype="f32", B=1, M=5, H=3, d=128, steps=2, L=33),
+    dict(dtype="f32", B=2, M=9, H=1, d=32, steps=8, L=1),
+    dict(dtype="bf16", B=1, M=1, H=1, d=64, steps=8, L=1),
+    dict(dtype="bf16", B=4, M=64, H=2, d=64, steps=4, L=64, parents="zipf", zipf_s=1.5),
+]
+
+
+@pytest.mark.parametrize("i", range(len(EDGE)))
+def test_edge_shapes_full_parity(gpu, i):
+    kw = dict(EDGE[i])
+    kw.setdefault("parents", "uniform")
+    wl = W.custom(name=f"edge{i}", **kw)
+    _log(f"[parity edge] {wl}")
+    dec = Decode(wl, 1 + i, gpu)
+    for t in range(wl.steps):
+        dec.run_step(t)
+    torch.cuda.synchronize()
+    _full_check(dec)
+
+
+def test_first_step_is_v_new_bitwise(gpu):
+    for dtype in ("bf16", "f32"):
+        wl = W.custom(dtype=dtype, B=2, M=40, H=3, d=64, steps=2, L=8)
+        dec = Decode(wl, 5, gpu)
+        rec = dec.run_step(0)
+        torch.cuda.synchronize()
+        assert torch.equal(rec["xs"], rec["vn"]), dtype
+
+
+def test_single_token_encoder_returns_v(gpu):
+    """L_b = 1: every beam of the request reads that token's value."""
+    for dtype in ("bf16", "f32"):
+        wl = W.custom(dtype=dtype, B=3, M=100, H=2, d=128, steps=1, L=1)
+        dec = Decode(wl, 6, gpu)
+        rec = dec.run_step(0)
+        torch.cuda.synchronize()
+        want = dec.enc_v.repeat_interleave(wl.M, dim=0)
+        assert torch.equal(rec["xc"], want), dtype
+
+
+def test_empty_request_gives_zero_rows(gpu):
+    wl = W.custom(dtype="bf16", B=3, M=20, H=2, d=64, steps=1, L=10)
+    inp = W.DecodeInputs(wl, 0, gpu)
+    ek, ev = inp.enc_kv
+    off = torch.tensor([0, 10, 10, 20], dtype=torch.int32, device=gpu)   # request 1 is empty
+    q = inp.step_tensor("q_cross", 0)
+    out = G.grace_cross_attn(q, ek, ev, off, wl.M)
+    torch.cuda.synchronize()
+    assert bool((out[20:40] == 0).all())
+    ref = oracle.cross_attn(_np(q), _np(ek), _np(ev), [0, 10, 10, 20], wl.M, 1 / 8)
+    assert np.max(np.abs(_np(out) - ref)) <= TOL["bf16"]
+
+
+def test_aliased_slab_append_matches_copy(gpu):
+    """k_new/v_new written straight into the pool slab: the copy is skipped, results equal."""
+    wl = W.custom(dtype="bf16", B=2, M=48, H=4, d=64, steps=3, L=16)
+    a = Decode(wl, 7, gpu)
+    for t in range(wl.steps):
+        a.run_step(t)
+    inp = a.inp
+    cache = G.KVCache(wl.B, wl.M, wl.H, wl.d, wl.steps, wl.torch_dtype, gpu)
+    for t in range(wl.steps):
+        ks, vs = cache.slab(t)
+        ks.copy_(inp.step_tensor("k_new", t))
+        vs.copy_(inp.step_tensor("v_new", t))
+        par = None if t == 0 else torch.from_numpy(a.parents[t]).to(gpu)
+        cache.append(t, ks, vs, par)
+        out = cache.attend(t, inp.step_tensor("q_self", t))
+        torch.cuda.synchronize()
+        assert torch.equal(out, a.steps[t]["xs"])
+        assert torch.equal(cache.table(t)[:, :t + 1], a.steps[t]["table"][:, :t + 1])
+
+
+def test_out_of_range_parent_sets_flag(gpu):
+    wl = W.custom(dtype="bf16", B=2, M=8, H=1, d=32, steps=2, L=4)
+    dec = Decode(wl, 8, gpu)
+    dec.run_step(0)
+    assert int(dec.cache.err_flag.item()) == 0
+    dec.parents[1] = dec.parents[1].copy()
+    dec.parents[1][3] = wl.M + 5
+    dec.run_step(1)
+    torch.cuda.synchronize()
+    assert int(dec.cache.err_flag.item()) == 1
+    # the bad row was clamped to the last beam of its request; the others are exact
+    tab = dec.steps[1]["table"].cpu().numpy()
+    assert tab[3, 0] == wl.M - 1
+
+
+def test_deterministic_and_relabelling_invariant(gpu):
+    wl = W.custom(dtype="bf16", B=2, M=96, H=2, d=64, steps=4, L=100, parents="zipf", zipf_s=1.2)
+    a = Decode(wl, 9, gpu)
+    b = Decode(wl, 9, gpu)
+    for t in range(wl.steps):
+        ra, rb = a.run_step(t), b.run_step(t)
+        torch.cuda.synchronize()
+        assert torch.equal(ra["xc"], rb["xc"]) and torch.equal(ra["xs"], rb["xs"])
+    # permute physical blocks, remap the table: self-attention output is unchanged
+    t = wl.steps - 1
+    nblk = wl.steps * wl.R
+    pi = torch.randperm(nblk, generator=torch.Generator().manual_seed(0)).to(gpu)
+    kflat = a.cache.k_pool.reshape(nblk, wl.H, wl.d)
+    vflat = a.cache.v_pool.reshape(nblk, wl.H, wl.d)
+    kperm = torch.empty_like(kflat)
+    vperm = torch.empty_like(vflat)
+    kperm[pi] = kflat
+    vperm[pi] = vflat
+    table = a.steps[t]["table"].clone()
+    table[:, :t + 1] = pi[table[:, :t + 1].long()].int()
+    out = G.grace_self_attn_step(a.steps[t]["qs"], kperm.reshape(a.cache.k_pool.shape),
+                                 vperm.reshape(a.cache.v_pool.shape), table, wl.B, wl.M, t)
+    torch.cuda.synchronize()
+    assert torch.equal(out, a.steps[t]["xs"])
+
+
+def test_empty_batch_is_noop(gpu):
+    q = torch.empty((0, 2, 64), dtype=torch.bfloat16, device=gpu)
+    kv = torch.zeros((4, 2, 64), dtype=torch.bfloat16, device=gpu)
+    off = torch.zeros(1, dtype=torch.int32, device=gpu)
+    out = G.grace_cross_attn(q, kv, kv, off, 0)
+    assert out.shape == (0, 2, 64)
