@@ -1,0 +1,273 @@
+#!/usr/bin/env python3
+"""Decode-step benchmark of the GRACE wide-beam attention hot path on one MI355X.
+
+A step is one decode step of one decoder layer's attention at step index
+t = k mod T: grace_cross_attn + grace_kv_append + grace_self_attn_step on the
+64 requests x 4096 beams workload (encoder length 1024, 16 heads x 64, bf16,
+Zipf(1.1) parents), with every input already resident in HBM.  The timed
+region covers K consecutive steps (cycling t = 0..T-1, i.e. K/T full decodes)
+bracketed by device synchronisation; per-kernel durations come from HIP events
+recorded on the stream the kernels run on.
+
+Prints one JSON line (last line of stdout).  Diagnostics go to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "µs per decode step (cross+self attn) at 64 req×4096 beams; MFMA % and HBM GB/s"
+WORKLOAD = "bf16_b64_m4096"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "cross_attn_bf16_b64_m4096_traffic.txt")
+CROSS_SRC = os.path.join(ROOT, "paper_2608_00938_amd", "csrc", "cross_attn.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def unique_ancestor_blocks(wl, parents, t):
+    """Distinct physical blocks at each prefix position j <= t over all rows (exact)."""
+    R, M = wl.R, wl.M
+    cur = np.arange(R, dtype=np.int64)
+    counts = [0] * (t + 1)
+    for j in range(t, -1, -1):
+        counts[j] = int(np.unique(cur).size)
+        if j > 0:
+            cur = (cur // M) * M + parents[j].astype(np.int64)[cur]
+    return counts
+
+
+def algorithmic(wl, sum_L, parents):
+    """Per-launch algorithmic work: cross flops, bytes of append and self per step t."""
+    s, E, R = wl.elem_bytes, wl.E, wl.R
+    slab = R * E * s
+    cross_flops = 4.0 * wl.H * wl.d * wl.M * sum_L
+    cross_bytes = 2 * slab + 2 * sum_L * E * s
+    append_b, self_b, self_logical = [], [], []
+    for t in range(wl.steps):
+        append_b.append(4 * slab + R * 4 * (1 if t > 0 else 0) + R * t * 4 + R * (t + 1) * 4)
+        uniq = unique_ancestor_blocks(wl, parents, t)
+        self_b.append(2 * slab + sum(2 * E * s * u for u in uniq) + R * (t + 1) * 4)
+        self_logical.append(2 * slab + 2 * (t + 1) * slab + R * (t + 1) * 4)
+    return cross_flops, cross_bytes, append_b, self_b, self_logical
+
+
+def read_traffic():
+    """HBM bytes per cross-attention launch measured by rocprofv3 counters, if the
+    kernel source is unchanged since they were taken; else None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    for ln in open(TRAFFIC_FILE):
+        if "=" in ln and not ln.lstrip().startswith("#"):
+            k, v = ln.split("=", 1)
+            vals[k.strip()] = v.strip()
+    src_hash = hashlib.sha256(open(CROSS_SRC, "rb").read()).hexdigest()[:16]
+    if vals.get("cross_attn_src_sha256_16") != src_hash:
+        return None
+    try:
+        return float(vals["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(wl, inp, parents, budget_s=12.0):
+    """Time the fp64 oracle on host cores on a bounded sample of one step at t=T-1:
+    whole requests (all beams and heads), added one at a time until the budget is
+    spent; scaled to the full step."""
+    import oracle
+    from threadpoolctl import threadpool_info
+
+    t = wl.steps - 1
+    scale = 1.0 / math.sqrt(wl.d)
+    ek, ev = inp.enc_kv
+    qc = inp.step_tensor("q_cross", t).cpu()
+    qs = inp.step_tensor("q_self", t).cpu()
+    steps_k = [inp.step_tensor("k_new", j).cpu() for j in range(t + 1)]
+    steps_v = [inp.step_tensor("v_new", j).cpu() for j in range(t + 1)]
+    ek, ev = ek.cpu(), ev.cpu()
+    off = inp.offsets
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    elapsed, nreq = 0.0, 0
+    while nreq < wl.B and elapsed < budget_s:
+        b = nreq
+        rows = np.arange(b * wl.M, (b + 1) * wl.M)
+        t0 = time.perf_counter()
+        oracle.cross_attn_request(qc[rows], ek[off[b]:off[b + 1]], ev[off[b]:off[b + 1]], scale)
+        tab = oracle.table_rows(rows, t, parents, wl.B, wl.M)
+        kpre = np.stack([steps_k[j][torch_index(tab[:, j] - j * wl.R)].double().numpy()
+                         for j in range(t + 1)], axis=1)
+        vpre = np.stack([steps_v[j][torch_index(tab[:, j] - j * wl.R)].double().numpy()
+                         for j in range(t + 1)], axis=1)
+        oracle.self_attn_rows(qs[rows], kpre, vpre, scale)
+        elapsed += time.perf_counter() - t0
+        nreq += 1
+    per_step_us = elapsed / nreq * wl.B * 1e6
+    return {"value": round(per_step_us, 1), "unit": "µs per decode step", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{nreq} of {wl.B} requests (all {wl.M} beams, {wl.H} heads), one step at "
+                      f"t={t}: cross-attention + table rows + self-attention, fp64 numpy; "
+                      f"{elapsed:.1f} s measured, scaled x{wl.B / nreq:.1f}"}
+
+
+def torch_index(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=40)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", default=WORKLOAD, help=argparse.SUPPRESS)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this hot path shards by request with no exchange, and "
+              f"this build runs on a single MI355X (asked for --gpus {args.gpus})", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_00938_amd import grace as G
+    from paper_2608_00938_amd import workloads as W
+
+    if not torch.cuda.is_available():
+        log("no GPU visible")
+        sys.exit(1)
+    G.library()   # fails loudly if the HIP library is not built
+    dev = torch.device("cuda:0")
+    props = torch.cuda.get_device_properties(dev)
+    log(f"device: {props.name} {getattr(props, 'gcnArchName', '')} CUs={props.multi_processor_count}")
+
+    wl = W.WORKLOADS[args.workload]
+    inp = W.DecodeInputs(wl, args.seed, dev)
+    ek, ev = inp.enc_kv
+    off = inp.offsets_tensor()
+    T = wl.steps
+    scale = 1.0 / math.sqrt(wl.d)
+    parents_np = [inp.parents(t) for t in range(T)]
+    t_gen = time.perf_counter()
+    steps = []
+    for t in range(T):
+        steps.append(dict(
+            qc=inp.step_tensor("q_cross", t), qs=inp.step_tensor("q_self", t),
+            kn=inp.step_tensor("k_new", t), vn=inp.step_tensor("v_new", t),
+            par=None if parents_np[t] is None else torch.from_numpy(parents_np[t]).to(dev),
+            xc=torch.empty((wl.R, wl.H, wl.d), dtype=wl.torch_dtype, device=dev),
+            xs=torch.empty((wl.R, wl.H, wl.d), dtype=wl.torch_dtype, device=dev)))
+    cache = G.KVCache(wl.B, wl.M, wl.H, wl.d, T, wl.torch_dtype, dev)
+    torch.cuda.synchronize()
+    log(f"inputs resident: {wl.name}, sum_L={inp.sum_L}, generated in {time.perf_counter() - t_gen:.1f} s")
+
+    stream = torch.cuda.current_stream(dev)
+    n_ev = args.steps
+    ev_c = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n_ev)]
+
+    def step(k, events=None):
+        t = k % T
+        s = steps[t]
+        if events:
+            events[0].record(stream)
+        G.grace_cross_attn(s["qc"], ek, ev, off, wl.M, scale, out=s["xc"])
+        if events:
+            events[1].record(stream)
+        cache.append(t, s["kn"], s["vn"], s["par"])
+        if events:
+            events[2].record(stream)
+        cache.attend(t, s["qs"], scale, out=s["xs"])
+        if events:
+            events[3].record(stream)
+
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+    # the warmup may end mid-decode; start the timed region at step index 0
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(k, ev_c[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    assert int(cache.err_flag.item()) == 0
+
+    per = {"cross": [], "append": [], "self": []}
+    per_t = {"append": [[] for _ in range(T)], "self": [[] for _ in range(T)]}
+    step_ms = []
+    for k in range(args.steps):
+        e = ev_c[k]
+        c, a, s_ = e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])
+        per["cross"].append(c)
+        per["append"].append(a)
+        per["self"].append(s_)
+        per_t["append"][k % T].append(a)
+        per_t["self"][k % T].append(s_)
+        step_ms.append(e[0].elapsed_time(e[3]))
+    ms_per_step = wall * 1e3 / args.steps
+
+    cross_flops, cross_bytes, append_b, self_b, self_logical = algorithmic(wl, inp.sum_L, parents_np)
+    cross_ms = float(np.mean(per["cross"]))
+    achieved = cross_flops / (cross_ms * 1e-3) / 1e12
+    traffic = read_traffic()
+    # HBM rooflines of the two gather/copy kernels: algorithmic bytes over the mean duration
+    t_used = [k % T for k in range(args.steps)]
+    app_bytes = float(np.mean([append_b[t] for t in t_used]))
+    self_bytes = float(np.mean([self_b[t] for t in t_used]))
+    app_ms, self_ms = float(np.mean(per["append"])), float(np.mean(per["self"]))
+
+    result = {
+        "metric": METRIC,
+        "value": round(ms_per_step * 1e3, 2),
+        "unit": "µs",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "requests": wl.B, "beams": wl.M, "encoder_len": wl.L,
+                   "heads": wl.H, "head_dim": wl.d, "decode_steps": T,
+                   "parents": f"zipf(s={wl.zipf_s}) over beams, per-(request,step) permutation",
+                   "step": "cross_attn + kv_append (copy into slab) + self_attn_step, t = k mod 4"},
+        "roofline": {"bound": "mfma", "kernel": "grace_cross_attn (cross_attn_bf16_kernel<64>)",
+                     "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
+                     "algorithmic_flops_per_launch": cross_flops,
+                     "algorithmic_bytes_per_launch": cross_bytes},
+        "kernels_us": {"cross_attn": round(cross_ms * 1e3, 2), "kv_append": round(app_ms * 1e3, 2),
+                       "self_attn_step": round(self_ms * 1e3, 2),
+                       "kv_append_by_step": [round(float(np.mean(x)) * 1e3, 2) for x in per_t["append"]],
+                       "self_attn_by_step": [round(float(np.mean(x)) * 1e3, 2) for x in per_t["self"]]},
+        "hbm": {"kv_append_GBs": round(app_bytes / (app_ms * 1e-3) / 1e9, 1),
+                "kv_append_frac": round(app_bytes / (app_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                "self_attn_GBs_unique": round(self_bytes / (self_ms * 1e-3) / 1e9, 1),
+                "self_attn_frac_unique": round(self_bytes / (self_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                "self_attn_GBs_logical": round(float(np.mean([self_logical[t] for t in t_used]))
+                                               / (self_ms * 1e-3) / 1e9, 1),
+                "peak_GBs": PEAK_HBM_GBS},
+        "event_step_ms_median": round(float(np.median(step_ms)), 4),
+    }
+    if not args.no_cpu_baseline:
+        log("timing the oracle on host cores ...")
+        result["cpu_baseline"] = cpu_baseline(wl, inp, parents_np)
+    print(json.dumps(result, ensure_ascii=False), flush=True)
+
+
+if __name__ == "__main__":
+    main()
