@@ -13,6 +13,10 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
+// 16-byte register chunk.  A native vector (not HIP's union-based uint4) so that
+// arrays of chunks stay in VGPRs.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 
@@ -41,26 +45,26 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 template <class T> struct Chunk;
 template <> struct Chunk<F32> {
   static constexpr int kElems = 4;
-  __device__ __forceinline__ static void unpack(const uint4& u, float* f) {
+  __device__ __forceinline__ static void unpack(const u32x4& u, float* f) {
     f[0] = __uint_as_float(u.x); f[1] = __uint_as_float(u.y);
     f[2] = __uint_as_float(u.z); f[3] = __uint_as_float(u.w);
   }
-  __device__ __forceinline__ static uint4 pack(const float* f) {
-    return make_uint4(__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
-                      __float_as_uint(f[3]));
+  __device__ __forceinline__ static u32x4 pack(const float* f) {
+    return u32x4{__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
+                 __float_as_uint(f[3])};
   }
 };
 template <> struct Chunk<BF16> {
   static constexpr int kElems = 8;
-  __device__ __forceinline__ static void unpack(const uint4& u, float* f) {
+  __device__ __forceinline__ static void unpack(const u32x4& u, float* f) {
     f[0] = __uint_as_float(u.x << 16); f[1] = __uint_as_float(u.x & 0xffff0000u);
     f[2] = __uint_as_float(u.y << 16); f[3] = __uint_as_float(u.y & 0xffff0000u);
     f[4] = __uint_as_float(u.z << 16); f[5] = __uint_as_float(u.z & 0xffff0000u);
     f[6] = __uint_as_float(u.w << 16); f[7] = __uint_as_float(u.w & 0xffff0000u);
   }
-  __device__ __forceinline__ static uint4 pack(const float* f) {
-    return make_uint4(pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]),
-                      pack_bf16x2(f[4], f[5]), pack_bf16x2(f[6], f[7]));
+  __device__ __forceinline__ static u32x4 pack(const float* f) {
+    return u32x4{pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]),
+                 pack_bf16x2(f[4], f[5]), pack_bf16x2(f[6], f[7])};
   }
 };
 

@@ -17,10 +17,10 @@ constexpr int kAppendThreads = 256;
 constexpr int kAppendUnroll = 4;  // 16-byte chunks in flight per thread and tensor
 
 __global__ void __launch_bounds__(kAppendThreads)
-kv_append_kernel(uint4* __restrict__ k_slab, uint4* __restrict__ v_slab,
+kv_append_kernel(u32x4* __restrict__ k_slab, u32x4* __restrict__ v_slab,
                  const int32_t* __restrict__ table_prev, int32_t* __restrict__ table_next,
-                 const int32_t* __restrict__ parents, const uint4* __restrict__ k_new,
-                 const uint4* __restrict__ v_new, int32_t R, int32_t M, int32_t T_max,
+                 const int32_t* __restrict__ parents, const u32x4* __restrict__ k_new,
+                 const u32x4* __restrict__ v_new, int32_t R, int32_t M, int32_t T_max,
                  int32_t step, int32_t rows_per_block, int32_t chunks_per_row, int32_t copy_k,
                  int32_t copy_v, int32_t* __restrict__ err_flag) {
   const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
@@ -51,7 +51,7 @@ kv_append_kernel(uint4* __restrict__ k_slab, uint4* __restrict__ v_slab,
   const int64_t base = r0 * chunks_per_row;
   const int64_t n = (int64_t)nrows * chunks_per_row;
   for (int64_t c0 = threadIdx.x; c0 < n; c0 += (int64_t)kAppendThreads * kAppendUnroll) {
-    uint4 kb[kAppendUnroll], vb[kAppendUnroll];
+    u32x4 kb[kAppendUnroll], vb[kAppendUnroll];
 #pragma unroll
     for (int u = 0; u < kAppendUnroll; ++u) {
       const int64_t c = c0 + (int64_t)u * kAppendThreads;
@@ -83,8 +83,8 @@ hipError_t launch_kv_append(void* k_slab, void* v_slab, const int32_t* table_pre
   if (rows_per_block > 256) rows_per_block = 256;
   const int64_t blocks = ((int64_t)R + rows_per_block - 1) / rows_per_block;
   hipLaunchKernelGGL(kv_append_kernel, dim3((unsigned)blocks), dim3(kAppendThreads), 0, stream,
-                     (uint4*)k_slab, (uint4*)v_slab, table_prev, table_next, parents,
-                     (const uint4*)k_new, (const uint4*)v_new, R, M, T_max, step, rows_per_block,
+                     (u32x4*)k_slab, (u32x4*)v_slab, table_prev, table_next, parents,
+                     (const u32x4*)k_new, (const u32x4*)v_new, R, M, T_max, step, rows_per_block,
                      chunks_per_row, (int32_t)copy_k, (int32_t)copy_v, err_flag);
   return hipGetLastError();
 }
@@ -103,16 +103,16 @@ constexpr int kSelfThreads = 256;
 
 template <class T, int D, int NT, int U>
 __global__ void __launch_bounds__(kSelfThreads)
-self_attn_kernel(const uint4* __restrict__ q, const uint4* __restrict__ k_pool,
-                 const uint4* __restrict__ v_pool, const int32_t* __restrict__ table,
-                 uint4* __restrict__ out, int64_t total_chunks, int32_t chunks_per_row,
+self_attn_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_pool,
+                 const u32x4* __restrict__ v_pool, const int32_t* __restrict__ table,
+                 u32x4* __restrict__ out, int64_t total_chunks, int32_t chunks_per_row,
                  int32_t T_max, uint32_t nblocks, float c_scale) {
   constexpr int VEC = Chunk<T>::kElems;
   constexpr int CH = D / VEC;  // chunks (= lanes) per head
   const int64_t first = ((int64_t)blockIdx.x * kSelfThreads + threadIdx.x);
   const int64_t stride_u = (int64_t)gridDim.x * kSelfThreads;
 
-  uint4 qc[U], kc[U][NT], vc[U][NT];
+  u32x4 qc[U], kc[U][NT], vc[U][NT];
   bool live[U];
 #pragma unroll
   for (int u = 0; u < U; ++u) {
@@ -183,8 +183,8 @@ static hipError_t launch_self_nt(const void* q, const void* k_pool, const void* 
   int64_t blocks = (waves_needed + (kSelfThreads / 64) - 1) / (kSelfThreads / 64);
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL((self_attn_kernel<T, D, NT, U>), dim3((unsigned)blocks), dim3(kSelfThreads),
-                     0, stream, (const uint4*)q, (const uint4*)k_pool, (const uint4*)v_pool, table,
-                     (uint4*)out, total_chunks, chunks_per_row, T_max, nblocks, c_scale);
+                     0, stream, (const u32x4*)q, (const u32x4*)k_pool, (const u32x4*)v_pool, table,
+                     (u32x4*)out, total_chunks, chunks_per_row, T_max, nblocks, c_scale);
   return hipGetLastError();
 }
 
