@@ -135,6 +135,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="run one device copy of this many MiB first (reference for HBM counters)")
     ap.add_argument("--workload", default=WORKLOAD, help=argparse.SUPPRESS)
     args = ap.parse_args()
     if args.gpus != 1:
@@ -173,6 +175,13 @@ def main():
     cache = G.KVCache(wl.B, wl.M, wl.H, wl.d, T, wl.torch_dtype, dev)
     torch.cuda.synchronize()
     log(f"inputs resident: {wl.name}, sum_L={inp.sum_L}, generated in {time.perf_counter() - t_gen:.1f} s")
+
+    if args.calib_copy_mib:
+        src = torch.empty(args.calib_copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     stream = torch.cuda.current_stream(dev)
     n_ev = args.steps
@@ -245,7 +254,7 @@ def main():
                    "heads": wl.H, "head_dim": wl.d, "decode_steps": T,
                    "parents": f"zipf(s={wl.zipf_s}) over beams, per-(request,step) permutation",
                    "step": "cross_attn + kv_append (copy into slab) + self_attn_step, t = k mod 4"},
-        "roofline": {"bound": "mfma", "kernel": "grace_cross_attn (cross_attn_bf16_kernel<64>)",
+        "roofline": {"bound": "mfma", "kernel": "grace_cross_attn (cross_attn_bf16_dual_kernel<64>)",
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
                      "algorithmic_flops_per_launch": cross_flops,
