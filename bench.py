@@ -2,8 +2,9 @@
 """Decode-step benchmark of the GRACE wide-beam attention hot path on one MI355X.
 
 A step is one decode step of one decoder layer's attention at step index
-t = k mod T: grace_cross_attn + grace_kv_append + grace_self_attn_step on the
-64 requests x 4096 beams workload (encoder length 1024, 16 heads x 64, bf16,
+t = k mod T: grace_cross_attn + grace_self_attn_step_fused (paged append and
+self-attention in one pass; ``--path split`` times grace_kv_append +
+grace_self_attn_step instead) on the 64 requests x 4096 beams workload (encoder length 1024, 16 heads x 64, bf16,
 Zipf(1.1) parents), with every input already resident in HBM.  The timed
 region covers K consecutive steps (cycling t = 0..T-1, i.e. K/T full decodes)
 bracketed by device synchronisation; per-kernel durations come from HIP events
@@ -56,13 +57,16 @@ def algorithmic(wl, sum_L, parents):
     slab = R * E * s
     cross_flops = 4.0 * wl.H * wl.d * wl.M * sum_L
     cross_bytes = 2 * slab + 2 * sum_L * E * s
-    append_b, self_b, self_logical = [], [], []
+    append_b, self_b, self_logical, fused_b = [], [], [], []
     for t in range(wl.steps):
-        append_b.append(4 * slab + R * 4 * (1 if t > 0 else 0) + R * t * 4 + R * (t + 1) * 4)
+        table_b = R * 4 * (1 if t > 0 else 0) + R * t * 4 + R * (t + 1) * 4
+        append_b.append(4 * slab + table_b)
         uniq = unique_ancestor_blocks(wl, parents, t)
         self_b.append(2 * slab + sum(2 * E * s * u for u in uniq) + R * (t + 1) * 4)
         self_logical.append(2 * slab + 2 * (t + 1) * slab + R * (t + 1) * 4)
-    return cross_flops, cross_bytes, append_b, self_b, self_logical
+        # fused: q, k_new, v_new read, slab k/v and out written, ancestors j < t read once
+        fused_b.append(6 * slab + sum(2 * E * s * u for u in uniq[:t]) + table_b)
+    return cross_flops, cross_bytes, append_b, self_b, self_logical, fused_b
 
 
 def read_traffic():
@@ -135,6 +139,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--path", choices=("fused", "split"), default="fused",
+                    help="self-attention as one fused append+attend call, or append then attend")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one device copy of this many MiB first (reference for HBM counters)")
     ap.add_argument("--workload", default=WORKLOAD, help=argparse.SUPPRESS)
@@ -187,6 +193,8 @@ def main():
     n_ev = args.steps
     ev_c = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n_ev)]
 
+    fused = args.path == "fused"
+
     def step(k, events=None):
         t = k % T
         s = steps[t]
@@ -195,6 +203,12 @@ def main():
         G.grace_cross_attn(s["qc"], ek, ev, off, wl.M, scale, out=s["xc"])
         if events:
             events[1].record(stream)
+        if fused:
+            cache.append_attend(t, s["qs"], s["kn"], s["vn"], s["par"], scale, out=s["xs"])
+            if events:
+                events[2].record(stream)
+                events[3].record(stream)
+            return
         cache.append(t, s["kn"], s["vn"], s["par"])
         if events:
             events[2].record(stream)
@@ -227,7 +241,8 @@ def main():
         step_ms.append(e[0].elapsed_time(e[3]))
     ms_per_step = wall * 1e3 / args.steps
 
-    cross_flops, cross_bytes, append_b, self_b, self_logical = algorithmic(wl, inp.sum_L, parents_np)
+    cross_flops, cross_bytes, append_b, self_b, self_logical, fused_b = algorithmic(
+        wl, inp.sum_L, parents_np)
     cross_ms = float(np.mean(per["cross"]))
     achieved = cross_flops / (cross_ms * 1e-3) / 1e12
     traffic = read_traffic()
@@ -236,7 +251,31 @@ def main():
     app_bytes = float(np.mean([append_b[t] for t in t_used]))
     self_bytes = float(np.mean([self_b[t] for t in t_used]))
     app_ms, self_ms = float(np.mean(per["append"])), float(np.mean(per["self"]))
+    fused_bytes = float(np.mean([fused_b[t] for t in t_used]))
 
+    if fused:
+        # the fused call is timed between events 1 and 2 (events 2 and 3 are back to back)
+        fused_ms = float(np.mean(per["append"]))
+        kernels_us = {"cross_attn": round(cross_ms * 1e3, 2),
+                      "self_attn_step_fused": round(fused_ms * 1e3, 2),
+                      "self_attn_fused_by_step": [round(float(np.mean(x)) * 1e3, 2)
+                                                  for x in per_t["append"]]}
+        hbm = {"self_attn_fused_GBs": round(fused_bytes / (fused_ms * 1e-3) / 1e9, 1),
+               "self_attn_fused_frac": round(fused_bytes / (fused_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+               "algorithmic_bytes_per_launch": round(fused_bytes),
+               "peak_GBs": PEAK_HBM_GBS}
+    else:
+        kernels_us = {"cross_attn": round(cross_ms * 1e3, 2), "kv_append": round(app_ms * 1e3, 2),
+                      "self_attn_step": round(self_ms * 1e3, 2),
+                      "kv_append_by_step": [round(float(np.mean(x)) * 1e3, 2) for x in per_t["append"]],
+                      "self_attn_by_step": [round(float(np.mean(x)) * 1e3, 2) for x in per_t["self"]]}
+        hbm = {"kv_append_GBs": round(app_bytes / (app_ms * 1e-3) / 1e9, 1),
+               "kv_append_frac": round(app_bytes / (app_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+               "self_attn_GBs_unique": round(self_bytes / (self_ms * 1e-3) / 1e9, 1),
+               "self_attn_frac_unique": round(self_bytes / (self_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+               "self_attn_GBs_logical": round(float(np.mean([self_logical[t] for t in t_used]))
+                                              / (self_ms * 1e-3) / 1e9, 1),
+               "peak_GBs": PEAK_HBM_GBS}
     result = {
         "metric": METRIC,
         "value": round(ms_per_step * 1e3, 2),
@@ -253,23 +292,16 @@ def main():
         "config": {"workload": wl.name, "requests": wl.B, "beams": wl.M, "encoder_len": wl.L,
                    "heads": wl.H, "head_dim": wl.d, "decode_steps": T,
                    "parents": f"zipf(s={wl.zipf_s}) over beams, per-(request,step) permutation",
-                   "step": "cross_attn + kv_append (copy into slab) + self_attn_step, t = k mod 4"},
+                   "step": ("cross_attn + self_attn_step_fused (append + attend)" if fused else
+                            "cross_attn + kv_append (copy into slab) + self_attn_step")
+                           + ", t = k mod 4"},
         "roofline": {"bound": "mfma", "kernel": "grace_cross_attn (cross_attn_bf16_dual_kernel<64>)",
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
                      "algorithmic_flops_per_launch": cross_flops,
                      "algorithmic_bytes_per_launch": cross_bytes},
-        "kernels_us": {"cross_attn": round(cross_ms * 1e3, 2), "kv_append": round(app_ms * 1e3, 2),
-                       "self_attn_step": round(self_ms * 1e3, 2),
-                       "kv_append_by_step": [round(float(np.mean(x)) * 1e3, 2) for x in per_t["append"]],
-                       "self_attn_by_step": [round(float(np.mean(x)) * 1e3, 2) for x in per_t["self"]]},
-        "hbm": {"kv_append_GBs": round(app_bytes / (app_ms * 1e-3) / 1e9, 1),
-                "kv_append_frac": round(app_bytes / (app_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
-                "self_attn_GBs_unique": round(self_bytes / (self_ms * 1e-3) / 1e9, 1),
-                "self_attn_frac_unique": round(self_bytes / (self_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
-                "self_attn_GBs_logical": round(float(np.mean([self_logical[t] for t in t_used]))
-                                               / (self_ms * 1e-3) / 1e9, 1),
-                "peak_GBs": PEAK_HBM_GBS},
+        "kernels_us": kernels_us,
+        "hbm": hbm,
         "event_step_ms_median": round(float(np.median(step_ms)), 4),
     }
     if not args.no_cpu_baseline:

@@ -10,7 +10,10 @@
  *                         parent's ids, the current token takes a fresh block
  *                         (Sec. 3.3, Sec. 5.3);
  *   grace_self_attn_step  each beam attends over its short paged Semantic-ID
- *                         prefix, positions 0..step (Sec. 5.2, Sec. 5.3).
+ *                         prefix, positions 0..step (Sec. 5.2, Sec. 5.3);
+ *   grace_self_attn_step_fused
+ *                         the previous two in one pass: table update, append
+ *                         and self-attention (Sec. 5.2 kernel fusion, Sec. 5.3).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -144,6 +147,47 @@ int32_t grace_self_attn_step(const void* q, const void* k_pool, const void* v_po
                              const int32_t* table, int32_t B, int32_t M, int32_t H, int32_t d,
                              int32_t T_max, int32_t step, float scale, int32_t dtype, void* out,
                              void* stream);
+
+/*
+ * Fused paged append and self-attention at decode step `step` (the paper's
+ * fused, paged self-attention: Sec. 5.2, Sec. 5.3).  One pass computes exactly
+ * what grace_kv_append followed by grace_self_attn_step on table_next computes:
+ *   table_next[i, j]    = table_prev[b*M + parents[i], j]   for 0 <= j < step
+ *   table_next[i, step] = step*R + i
+ *   k_pool[step, i] = k_new[i],  v_pool[step, i] = v_new[i]
+ *   out[i, h, :] = sum_j softmax_j(scale * <q[i, h, :], K_j[h, :]>) * V_j[h, :],
+ *     j = 0 .. step, where K_j/V_j for j < step are the blocks table_next[i, j]
+ *     and K_step/V_step are k_new[i]/v_new[i] (taken from the inputs, not
+ *     re-read from the pool).
+ * Each (row, head) reads its ancestors' blocks once and its current token
+ * once, so the slab written by the append is never read back in this step.
+ *
+ *   q               device, [B*M, H, d], dtype
+ *   k_new, v_new    device, [B*M, H, d], dtype; as for grace_kv_append (a pointer
+ *                   equal to its pool's slab `step` skips that copy)
+ *   k_pool, v_pool  device, [T_max, B*M, H, d], dtype; slabs 0..step-1 read,
+ *                   slab `step` written
+ *   table_prev      device, int32 [B*M, T_max]; read for step > 0 (NULL allowed at step 0)
+ *   table_next      device, int32 [B*M, T_max]; columns 0..step written
+ *   parents         device, int32 [B*M]; as for grace_kv_append (NULL allowed at step 0)
+ *   B, M, H, d      as for grace_cross_attn
+ *   T_max, step     as for grace_kv_append
+ *   scale           softmax scale, finite and > 0
+ *   dtype           GRACE_F32 or GRACE_BF16
+ *   out             device, [B*M, H, d], dtype
+ *   err_flag        device int32 or NULL; set to 1 when a parent was out of range
+ *                   (it is then clamped into [0, M)), never cleared by the library
+ *   stream          hipStream_t
+ * Every written range (out, table_next, and each slab that is copied) must be
+ * disjoint from every other written range and from every range read (q, k_new,
+ * v_new, table_prev, parents, pool slabs 0..step-1); otherwise GRACE_ERR_ALIAS.
+ */
+int32_t grace_self_attn_step_fused(const void* q, const void* k_new, const void* v_new,
+                                   void* k_pool, void* v_pool, const int32_t* table_prev,
+                                   int32_t* table_next, const int32_t* parents, int32_t B,
+                                   int32_t M, int32_t H, int32_t d, int32_t T_max, int32_t step,
+                                   float scale, int32_t dtype, void* out, int32_t* err_flag,
+                                   void* stream);
 
 /* Human-readable name of a status code (static storage; never NULL). */
 const char* grace_status_string(int32_t status);

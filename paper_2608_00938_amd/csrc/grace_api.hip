@@ -137,4 +137,51 @@ int32_t grace_self_attn_step(const void* q, const void* k_pool, const void* v_po
                                                  (hipStream_t)stream));
 }
 
+int32_t grace_self_attn_step_fused(const void* q, const void* k_new, const void* v_new,
+                                   void* k_pool, void* v_pool, const int32_t* table_prev,
+                                   int32_t* table_next, const int32_t* parents, int32_t B,
+                                   int32_t M, int32_t H, int32_t d, int32_t T_max, int32_t step,
+                                   float scale, int32_t dtype, void* out, int32_t* err_flag,
+                                   void* stream) {
+  int64_t R, row_bytes;
+  int32_t st = check_shape(B, M, H, d, dtype, R, row_bytes);
+  if (st != GRACE_OK) return st;
+  if (T_max < 1 || T_max > 8 || step < 0 || step >= T_max) return GRACE_ERR_SHAPE;
+  if ((int64_t)T_max * R >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
+  if (!good_scale(scale)) return GRACE_ERR_SHAPE;
+  if (R == 0) return GRACE_OK;
+  if (!q || !k_new || !v_new || !k_pool || !v_pool || !table_next || !out) return GRACE_ERR_NULL;
+  if (step > 0 && (!table_prev || !parents)) return GRACE_ERR_NULL;
+  const int64_t slab = R * row_bytes, table_bytes = R * T_max * 4;
+  char* k_slab = (char*)k_pool + step * slab;
+  char* v_slab = (char*)v_pool + step * slab;
+  const bool copy_k = k_new != (const void*)k_slab;
+  const bool copy_v = v_new != (const void*)v_slab;
+  struct Range {
+    const void* p;
+    int64_t n;
+  };
+  // Written ranges, then read ranges.  An uncopied slab is read (as k_new/v_new), not written.
+  const Range writes[4] = {{out, slab},
+                           {table_next, table_bytes},
+                           {copy_k ? k_slab : nullptr, copy_k ? slab : 0},
+                           {copy_v ? v_slab : nullptr, copy_v ? slab : 0}};
+  const Range reads[7] = {{q, slab},
+                          {k_new, slab},
+                          {v_new, slab},
+                          {step > 0 ? table_prev : nullptr, step > 0 ? table_bytes : 0},
+                          {step > 0 ? parents : nullptr, step > 0 ? R * 4 : 0},
+                          {k_pool, step * slab},
+                          {v_pool, step * slab}};
+  for (int i = 0; i < 4; ++i) {
+    for (int j = i + 1; j < 4; ++j)
+      if (overlaps(writes[i].p, writes[i].n, writes[j].p, writes[j].n)) return GRACE_ERR_ALIAS;
+    for (int j = 0; j < 7; ++j)
+      if (overlaps(writes[i].p, writes[i].n, reads[j].p, reads[j].n)) return GRACE_ERR_ALIAS;
+  }
+  return hip_status(grace::launch_self_attn_fused(
+      q, k_new, v_new, k_pool, v_pool, table_prev, table_next, parents, out, (int32_t)R, M, H, d,
+      T_max, step, scale, dtype == GRACE_BF16, copy_k, copy_v, err_flag, (hipStream_t)stream));
+}
+
 }  // extern "C"

@@ -25,4 +25,13 @@ hipError_t launch_self_attn_step(const void* q, const void* k_pool, const void* 
                                  int32_t T_max, int32_t step, float scale, bool bf16,
                                  hipStream_t stream);
 
+// Fused append + attend: table update, slab write (unless aliased) and
+// self-attention over step+1 tokens in one pass.
+hipError_t launch_self_attn_fused(const void* q, const void* k_new, const void* v_new,
+                                  void* k_pool, void* v_pool, const int32_t* table_prev,
+                                  int32_t* table_next, const int32_t* parents, void* out, int32_t R,
+                                  int32_t M, int32_t H, int32_t d, int32_t T_max, int32_t step,
+                                  float scale, bool bf16, bool copy_k, bool copy_v,
+                                  int32_t* err_flag, hipStream_t stream);
+
 }  // namespace grace

@@ -97,18 +97,73 @@ hipError_t launch_kv_append(void* k_slab, void* v_slab, const int32_t* table_pre
 // head never straddles two waves).  Lane group sums give the scores, every
 // lane of the group keeps all NT scores, and the softmax over NT <= 8 values
 // runs in registers.  Each lane issues all of its q/K/V loads before any math.
+// When a row is a whole number of waves (H*d*elem a multiple of 1 KiB), the
+// row index is wave-uniform and the table/parent reads become scalar loads.
 // ---------------------------------------------------------------------------
 
 constexpr int kSelfThreads = 256;
 
-template <class T, int D, int NT, int U>
+// Output chunk of one (row, head-slice): softmax over NT scores, weighted V.
+template <class T, int D, int NT>
+__device__ __forceinline__ u32x4 attend_chunk(const u32x4& qc, const u32x4* kc, const u32x4* vc,
+                                              float c_scale) {
+  constexpr int VEC = Chunk<T>::kElems;
+  constexpr int CH = D / VEC;  // chunks (= lanes) per head
+  float qf[VEC];
+  Chunk<T>::unpack(qc, qf);
+  float s[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    float kf[VEC];
+    Chunk<T>::unpack(kc[j], kf);
+    float acc = 0.f;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc = __builtin_fmaf(qf[e], kf[e], acc);
+    s[j] = group_sum<CH>(acc);
+  }
+  float mx = s[0];
+#pragma unroll
+  for (int j = 1; j < NT; ++j) mx = fmaxf(mx, s[j]);
+  float p[NT], l = 0.f;
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    p[j] = fast_exp2((s[j] - mx) * c_scale);
+    l += p[j];
+  }
+  const float inv = 1.0f / l;
+  float o[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) o[e] = 0.f;
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    float vf[VEC];
+    Chunk<T>::unpack(vc[j], vf);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) o[e] = __builtin_fmaf(p[j], vf[e], o[e]);
+  }
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) o[e] *= inv;
+  return Chunk<T>::pack(o);
+}
+
+// Row of chunk g; wave-uniform (scalar) when rows are whole waves.
+template <bool UNIFORM>
+__device__ __forceinline__ int64_t row_of(int64_t g, int32_t chunks_per_row) {
+  const int64_t r = g / chunks_per_row;
+  if constexpr (UNIFORM) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)r);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(r >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+  }
+  return r;
+}
+
+template <class T, int D, int NT, int U, bool UNIFORM>
 __global__ void __launch_bounds__(kSelfThreads)
 self_attn_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_pool,
                  const u32x4* __restrict__ v_pool, const int32_t* __restrict__ table,
                  u32x4* __restrict__ out, int64_t total_chunks, int32_t chunks_per_row,
                  int32_t T_max, uint32_t nblocks, float c_scale) {
-  constexpr int VEC = Chunk<T>::kElems;
-  constexpr int CH = D / VEC;  // chunks (= lanes) per head
   const int64_t first = ((int64_t)blockIdx.x * kSelfThreads + threadIdx.x);
   const int64_t stride_u = (int64_t)gridDim.x * kSelfThreads;
 
@@ -119,9 +174,9 @@ self_attn_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_pool,
     const int64_t g = first + u * stride_u;
     live[u] = g < total_chunks;
     const int64_t gg = live[u] ? g : 0;
-    const int64_t r = gg / chunks_per_row;
+    const int64_t r = row_of<UNIFORM>(gg, chunks_per_row);
     const int32_t c = (int32_t)(gg - r * chunks_per_row);
-    qc[u] = q[gg];
+    qc[u] = __builtin_nontemporal_load(&q[gg]);
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
       uint32_t id = (uint32_t)table[r * T_max + j];
@@ -131,90 +186,153 @@ self_attn_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_pool,
       vc[u][j] = v_pool[off];
     }
   }
-
 #pragma unroll
   for (int u = 0; u < U; ++u) {
-    float qf[VEC];
-    Chunk<T>::unpack(qc[u], qf);
-    float s[NT];
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      float kf[VEC];
-      Chunk<T>::unpack(kc[u][j], kf);
-      float acc = 0.f;
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) acc = __builtin_fmaf(qf[e], kf[e], acc);
-      s[j] = group_sum<CH>(acc);
-    }
-    float mx = s[0];
-#pragma unroll
-    for (int j = 1; j < NT; ++j) mx = fmaxf(mx, s[j]);
-    float p[NT], l = 0.f;
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      p[j] = fast_exp2((s[j] - mx) * c_scale);
-      l += p[j];
-    }
-    const float inv = 1.0f / l;
-    float o[VEC];
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) o[e] = 0.f;
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      float vf[VEC];
-      Chunk<T>::unpack(vc[u][j], vf);
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) o[e] = __builtin_fmaf(p[j], vf[e], o[e]);
-    }
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) o[e] *= inv;
-    if (live[u]) out[first + u * stride_u] = Chunk<T>::pack(o);
+    const u32x4 o = attend_chunk<T, D, NT>(qc[u], kc[u], vc[u], c_scale);
+    if (live[u]) __builtin_nontemporal_store(o, &out[first + u * stride_u]);
   }
 }
 
-template <class T, int D, int NT>
-static hipError_t launch_self_nt(const void* q, const void* k_pool, const void* v_pool,
-                                 const int32_t* table, void* out, int64_t total_chunks,
-                                 int32_t chunks_per_row, int32_t T_max, uint32_t nblocks,
-                                 float c_scale, hipStream_t stream) {
+// Fused append + attend (the paper's fused and paged self-attention): each row
+// takes its parent's block ids for positions < step, writes them and its fresh
+// block id to table_next, stores the current token's k/v into slab `step`, and
+// attends over the ancestors' blocks plus the current token held in registers.
+template <class T, int D, int NT, int U, bool UNIFORM>
+__global__ void __launch_bounds__(kSelfThreads)
+self_attn_fused_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_new,
+                       const u32x4* __restrict__ v_new, u32x4* __restrict__ k_pool,
+                       u32x4* __restrict__ v_pool, const int32_t* __restrict__ table_prev,
+                       int32_t* __restrict__ table_next, const int32_t* __restrict__ parents,
+                       u32x4* __restrict__ out, int64_t total_chunks, int32_t chunks_per_row,
+                       int32_t R, int32_t M, int32_t T_max, uint32_t nblocks, float c_scale,
+                       int32_t copy_k, int32_t copy_v, int32_t* __restrict__ err_flag) {
+  constexpr int STEP = NT - 1;
+  const int64_t first = ((int64_t)blockIdx.x * kSelfThreads + threadIdx.x);
+  const int64_t stride_u = (int64_t)gridDim.x * kSelfThreads;
+  const int64_t slab = (int64_t)STEP * R * chunks_per_row;   // chunk offset of slab `step`
+
+  u32x4 qc[U], kc[U][NT], vc[U][NT];
+  int32_t ids[U][NT > 1 ? NT - 1 : 1];
+  int64_t rows[U];
+  int32_t cols[U];
+  bool live[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t g = first + u * stride_u;
+    live[u] = g < total_chunks;
+    const int64_t gg = live[u] ? g : 0;
+    const int64_t r = row_of<UNIFORM>(gg, chunks_per_row);
+    const int32_t c = (int32_t)(gg - r * chunks_per_row);
+    rows[u] = r;
+    cols[u] = c;
+    qc[u] = __builtin_nontemporal_load(&q[gg]);
+    kc[u][STEP] = __builtin_nontemporal_load(&k_new[gg]);
+    vc[u][STEP] = __builtin_nontemporal_load(&v_new[gg]);
+    if constexpr (STEP > 0) {
+      int32_t p = parents[r];
+      if (p < 0 || p >= M) {
+        if (live[u] && err_flag) *err_flag = 1;
+        p = p < 0 ? 0 : M - 1;
+      }
+      const int64_t src = (r / M) * M + p;
+#pragma unroll
+      for (int j = 0; j < STEP; ++j) {
+        uint32_t id = (uint32_t)table_prev[src * T_max + j];
+        ids[u][j] = (int32_t)id;
+        id = id < nblocks ? id : nblocks - 1;
+        const int64_t off = (int64_t)id * chunks_per_row + c;
+        kc[u][j] = k_pool[off];
+        vc[u][j] = v_pool[off];
+      }
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    if (!live[u]) continue;
+    const int64_t g = first + u * stride_u;
+    if (copy_k) k_pool[slab + g] = kc[u][STEP];
+    if (copy_v) v_pool[slab + g] = vc[u][STEP];
+    const int32_t c = cols[u];
+    if (c <= STEP) {
+      int32_t id = (int32_t)(STEP * R + rows[u]);
+      if constexpr (STEP > 0) {
+#pragma unroll
+        for (int j = 0; j < STEP; ++j)
+          if (c == j) id = ids[u][j];
+      }
+      table_next[rows[u] * T_max + c] = id;
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const u32x4 o = attend_chunk<T, D, NT>(qc[u], kc[u], vc[u], c_scale);
+    if (live[u]) __builtin_nontemporal_store(o, &out[first + u * stride_u]);
+  }
+}
+
+struct SelfArgs {
+  const void* q;
+  const void* k_new;
+  const void* v_new;
+  void* k_pool;
+  void* v_pool;
+  const int32_t* table_prev;  // fused: parents' rows; plain: the table to read
+  int32_t* table_next;
+  const int32_t* parents;
+  void* out;
+  int64_t total_chunks;
+  int32_t chunks_per_row, R, M, T_max;
+  uint32_t nblocks;
+  float c_scale;
+  int32_t copy_k, copy_v;
+  int32_t* err_flag;
+};
+
+template <bool FUSED, class T, int D, int NT>
+static hipError_t launch_self_nt(const SelfArgs& a, hipStream_t stream) {
   // Two chunks per lane keep 2*(2*NT+1) 16-byte loads in flight per lane.
   constexpr int U = NT <= 4 ? 2 : 1;
-  int64_t waves_needed = (total_chunks + 64 * U - 1) / (64 * U);
+  int64_t waves_needed = (a.total_chunks + 64 * U - 1) / (64 * U);
   int64_t blocks = (waves_needed + (kSelfThreads / 64) - 1) / (kSelfThreads / 64);
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL((self_attn_kernel<T, D, NT, U>), dim3((unsigned)blocks), dim3(kSelfThreads),
-                     0, stream, (const u32x4*)q, (const u32x4*)k_pool, (const u32x4*)v_pool, table,
-                     (u32x4*)out, total_chunks, chunks_per_row, T_max, nblocks, c_scale);
+  const bool uniform = a.chunks_per_row % 64 == 0;
+#define GRACE_GO(UNI)                                                                               \
+  if constexpr (FUSED) {                                                                           \
+    hipLaunchKernelGGL((self_attn_fused_kernel<T, D, NT, U, UNI>), dim3((unsigned)blocks),         \
+                       dim3(kSelfThreads), 0, stream, (const u32x4*)a.q, (const u32x4*)a.k_new,    \
+                       (const u32x4*)a.v_new, (u32x4*)a.k_pool, (u32x4*)a.v_pool, a.table_prev,    \
+                       a.table_next, a.parents, (u32x4*)a.out, a.total_chunks, a.chunks_per_row,    \
+                       a.R, a.M, a.T_max, a.nblocks, a.c_scale, a.copy_k, a.copy_v, a.err_flag);   \
+  } else {                                                                                         \
+    hipLaunchKernelGGL((self_attn_kernel<T, D, NT, U, UNI>), dim3((unsigned)blocks),               \
+                       dim3(kSelfThreads), 0, stream, (const u32x4*)a.q, (const u32x4*)a.k_pool,   \
+                       (const u32x4*)a.v_pool, a.table_prev, (u32x4*)a.out, a.total_chunks,         \
+                       a.chunks_per_row, a.T_max, a.nblocks, a.c_scale);                           \
+  }
+  if (uniform) {
+    GRACE_GO(true)
+  } else {
+    GRACE_GO(false)
+  }
+#undef GRACE_GO
   return hipGetLastError();
 }
 
-template <class T, int D>
-static hipError_t launch_self_d(const void* q, const void* k_pool, const void* v_pool,
-                                const int32_t* table, void* out, int64_t total_chunks,
-                                int32_t chunks_per_row, int32_t T_max, int32_t step,
-                                uint32_t nblocks, float c_scale, hipStream_t stream) {
+template <bool FUSED, class T, int D>
+static hipError_t launch_self_d(const SelfArgs& a, int32_t step, hipStream_t stream) {
   switch (step + 1) {
 #define GRACE_NT(n) \
-  case n: return launch_self_nt<T, D, n>(q, k_pool, v_pool, table, out, total_chunks, \
-                                         chunks_per_row, T_max, nblocks, c_scale, stream);
+  case n: return launch_self_nt<FUSED, T, D, n>(a, stream);
     GRACE_NT(1) GRACE_NT(2) GRACE_NT(3) GRACE_NT(4) GRACE_NT(5) GRACE_NT(6) GRACE_NT(7) GRACE_NT(8)
 #undef GRACE_NT
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_self_attn_step(const void* q, const void* k_pool, const void* v_pool,
-                                 const int32_t* table, void* out, int32_t R, int32_t H, int32_t d,
-                                 int32_t T_max, int32_t step, float scale, bool bf16,
-                                 hipStream_t stream) {
-  const int32_t elem = bf16 ? 2 : 4;
-  const int32_t chunks_per_row = H * d * elem / 16;
-  const int64_t total_chunks = (int64_t)R * chunks_per_row;
-  const uint32_t nblocks = (uint32_t)((int64_t)T_max * R);
-  const float c = scale * kLog2e;
-#define GRACE_SELF(TT, DD) \
-  return launch_self_d<TT, DD>(q, k_pool, v_pool, table, out, total_chunks, chunks_per_row, \
-                               T_max, step, nblocks, c, stream)
+template <bool FUSED>
+static hipError_t launch_self_any(const SelfArgs& a, int32_t d, int32_t step, bool bf16,
+                                  hipStream_t stream) {
+#define GRACE_SELF(TT, DD) return launch_self_d<FUSED, TT, DD>(a, step, stream)
   if (bf16) {
     if (d == 32) GRACE_SELF(BF16, 32);
     if (d == 64) GRACE_SELF(BF16, 64);
@@ -226,6 +344,56 @@ hipError_t launch_self_attn_step(const void* q, const void* k_pool, const void* 
   }
 #undef GRACE_SELF
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_self_attn_step(const void* q, const void* k_pool, const void* v_pool,
+                                 const int32_t* table, void* out, int32_t R, int32_t H, int32_t d,
+                                 int32_t T_max, int32_t step, float scale, bool bf16,
+                                 hipStream_t stream) {
+  SelfArgs a = {};
+  const int32_t elem = bf16 ? 2 : 4;
+  a.q = q;
+  a.k_pool = const_cast<void*>(k_pool);
+  a.v_pool = const_cast<void*>(v_pool);
+  a.table_prev = table;
+  a.out = out;
+  a.chunks_per_row = H * d * elem / 16;
+  a.total_chunks = (int64_t)R * a.chunks_per_row;
+  a.R = R;
+  a.T_max = T_max;
+  a.nblocks = (uint32_t)((int64_t)T_max * R);
+  a.c_scale = scale * kLog2e;
+  return launch_self_any<false>(a, d, step, bf16, stream);
+}
+
+hipError_t launch_self_attn_fused(const void* q, const void* k_new, const void* v_new,
+                                  void* k_pool, void* v_pool, const int32_t* table_prev,
+                                  int32_t* table_next, const int32_t* parents, void* out, int32_t R,
+                                  int32_t M, int32_t H, int32_t d, int32_t T_max, int32_t step,
+                                  float scale, bool bf16, bool copy_k, bool copy_v,
+                                  int32_t* err_flag, hipStream_t stream) {
+  SelfArgs a = {};
+  const int32_t elem = bf16 ? 2 : 4;
+  a.q = q;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.k_pool = k_pool;
+  a.v_pool = v_pool;
+  a.table_prev = table_prev;
+  a.table_next = table_next;
+  a.parents = parents;
+  a.out = out;
+  a.chunks_per_row = H * d * elem / 16;
+  a.total_chunks = (int64_t)R * a.chunks_per_row;
+  a.R = R;
+  a.M = M;
+  a.T_max = T_max;
+  a.nblocks = (uint32_t)((int64_t)T_max * R);
+  a.c_scale = scale * kLog2e;
+  a.copy_k = copy_k;
+  a.copy_v = copy_v;
+  a.err_flag = err_flag;
+  return launch_self_any<true>(a, d, step, bf16, stream);
 }
 
 }  // namespace grace

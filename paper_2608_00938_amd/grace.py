@@ -1,6 +1,6 @@
 """Python binding of libgrace.so (argument marshalling only).
 
-The three entry points keep their C names and take torch tensors that already
+The entry points keep their C names and take torch tensors that already
 live on the GPU; each call passes raw device pointers, sizes, the dtype code and
 the current HIP stream to the library and turns a non-zero status into
 :class:`GraceError`.  Every step of the computation runs in the library's HIP
@@ -31,6 +31,10 @@ _SIGNATURES = {
                         _c_void_p, _c_void_p],
     "grace_self_attn_step": [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_int, _c_int, _c_int,
                              _c_int, _c_int, _c_int, _c_float, _c_int, _c_void_p, _c_void_p],
+    "grace_self_attn_step_fused": [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+                                   _c_void_p, _c_void_p, _c_void_p, _c_int, _c_int, _c_int,
+                                   _c_int, _c_int, _c_int, _c_float, _c_int, _c_void_p, _c_void_p,
+                                   _c_void_p],
     "grace_status_string": [_c_int],
     "grace_last_hip_error": [],
     "grace_abi_version": [],
@@ -132,6 +136,25 @@ def grace_self_attn_step(q, k_pool, v_pool, table, B: int, M: int, step: int,
     return out
 
 
+def grace_self_attn_step_fused(q, k_new, v_new, k_pool, v_pool, table_prev, table_next, parents,
+                               B: int, M: int, step: int, scale: float | None = None, out=None,
+                               err_flag=None):
+    """Paged append and self-attention in one pass: writes table_next and slab
+    ``step`` of the pools like :func:`grace_kv_append`, returns the attention of
+    :func:`grace_self_attn_step` over table_next [B*M, H, d]."""
+    _contig(q, k_new, v_new, k_pool, v_pool, table_prev, table_next, parents, out)
+    T_max, R, H, d = k_pool.shape
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    if out is None:
+        out = torch.empty_like(q)
+    st = library().grace_self_attn_step_fused(
+        _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_pool), _ptr(v_pool), _ptr(table_prev),
+        _ptr(table_next), _ptr(parents), B, M, H, d, T_max, step, scale, _dtype_code(q), _ptr(out),
+        _ptr(err_flag), _stream(q))
+    _check(st, "grace_self_attn_step_fused")
+    return out
+
+
 class KVCache:
     """Caller-side storage of the paged self-attention cache: the two pools and
     a pair of block tables used alternately (the update reads one, writes the
@@ -161,3 +184,11 @@ class KVCache:
     def attend(self, step: int, q, scale: float | None = None, out=None):
         return grace_self_attn_step(q, self.k_pool, self.v_pool, self.table(step), self.B, self.M,
                                     step, scale=scale, out=out)
+
+    def append_attend(self, step: int, q, k_new, v_new, parents=None, scale: float | None = None,
+                      out=None):
+        """:meth:`append` then :meth:`attend`, as one fused pass."""
+        return grace_self_attn_step_fused(q, k_new, v_new, self.k_pool, self.v_pool,
+                                          self.tables[(step + 1) % 2], self.tables[step % 2],
+                                          parents, self.B, self.M, step, scale=scale, out=out,
+                                          err_flag=self.err_flag)

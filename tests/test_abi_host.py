@@ -28,7 +28,8 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    for n in ("grace_cross_attn", "grace_kv_append", "grace_self_attn_step"):
+    for n in ("grace_cross_attn", "grace_kv_append", "grace_self_attn_step",
+              "grace_self_attn_step_fused"):
         assert n in names
 
 
@@ -112,6 +113,41 @@ def test_kv_append_rejects(kw, status):
 ])
 def test_self_attn_rejects(kw, status):
     assert selfattn(**kw) == status
+
+
+def fused(**kw):
+    # Slab = B*M*H*d*2 = 2048 bytes; pools span 4 slabs.
+    a = dict(q=ctypes.c_void_p(0x100000), kn=ctypes.c_void_p(0x200000), vn=ctypes.c_void_p(0x300000),
+             kp=ctypes.c_void_p(0x400000), vp=ctypes.c_void_p(0x500000), tp=ctypes.c_void_p(0x600000),
+             tn=ctypes.c_void_p(0x700000), par=ctypes.c_void_p(0x800000), B=2, M=4, H=2, d=64, T=4,
+             step=1, scale=0.125, dtype=1, out=ctypes.c_void_p(0x900000), err=None, stream=None)
+    a.update(kw)
+    return G.library().grace_self_attn_step_fused(
+        a["q"], a["kn"], a["vn"], a["kp"], a["vp"], a["tp"], a["tn"], a["par"], a["B"], a["M"],
+        a["H"], a["d"], a["T"], a["step"], a["scale"], a["dtype"], a["out"], a["err"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(T=9), G.GRACE_ERR_SHAPE), (dict(step=4), G.GRACE_ERR_SHAPE),
+    (dict(step=-1), G.GRACE_ERR_SHAPE), (dict(scale=math.nan), G.GRACE_ERR_SHAPE),
+    (dict(d=16), G.GRACE_ERR_UNSUPPORTED), (dict(dtype=3), G.GRACE_ERR_UNSUPPORTED),
+    (dict(q=None), G.GRACE_ERR_NULL), (dict(kn=None), G.GRACE_ERR_NULL),
+    (dict(vp=None), G.GRACE_ERR_NULL), (dict(tn=None), G.GRACE_ERR_NULL),
+    (dict(out=None), G.GRACE_ERR_NULL), (dict(tp=None), G.GRACE_ERR_NULL),
+    (dict(par=None), G.GRACE_ERR_NULL),
+    (dict(tn=ctypes.c_void_p(0x600000)), G.GRACE_ERR_ALIAS),            # table_next == table_prev
+    (dict(tn=ctypes.c_void_p(0x800000 - 8)), G.GRACE_ERR_ALIAS),        # table_next over parents
+    (dict(out=ctypes.c_void_p(0x100000 + 64)), G.GRACE_ERR_ALIAS),      # out over q
+    (dict(out=ctypes.c_void_p(0x700000)), G.GRACE_ERR_ALIAS),           # out == table_next
+    (dict(out=ctypes.c_void_p(0x400000 + 16)), G.GRACE_ERR_ALIAS),      # out over read slab 0
+    (dict(q=ctypes.c_void_p(0x400000 + 2048 + 64)), G.GRACE_ERR_ALIAS),  # q inside written slab 1
+    (dict(kn=ctypes.c_void_p(0x400000 + 2048 + 64)), G.GRACE_ERR_ALIAS),  # k_new inside slab 1
+    (dict(kn=ctypes.c_void_p(0x500000 + 2048)), G.GRACE_ERR_ALIAS),     # k_new is v's slab 1
+    (dict(tp=None, par=None, step=0, B=0), G.GRACE_OK),
+    (dict(M=0), G.GRACE_OK),
+])
+def test_self_attn_fused_rejects(kw, status):
+    assert fused(**kw) == status
 
 
 def test_binding_raises_without_library(monkeypatch, tmp_path):

@@ -32,10 +32,11 @@ def _np(t):
 
 
 class Decode:
-    """Runs the full decode of a workload on the GPU, one call per entry point per step."""
+    """Runs the full decode of a workload on the GPU, one call per entry point per
+    step; with ``fused`` the append and the self-attention are one fused call."""
 
-    def __init__(self, wl, seed, device, keep_inputs=True):
-        self.wl, self.seed = wl, seed
+    def __init__(self, wl, seed, device, fused=False):
+        self.wl, self.seed, self.fused = wl, seed, fused
         self.inp = W.DecodeInputs(wl, seed, device)
         self.enc_k, self.enc_v = self.inp.enc_kv
         self.off = self.inp.offsets_tensor()
@@ -52,8 +53,11 @@ class Decode:
         vn = inp.step_tensor("v_new", t)
         par = None if self.parents[t] is None else torch.from_numpy(self.parents[t]).to(qc.device)
         xc = G.grace_cross_attn(qc, self.enc_k, self.enc_v, self.off, wl.M, self.scale)
-        self.cache.append(t, kn, vn, par)
-        xs = self.cache.attend(t, qs, self.scale)
+        if self.fused:
+            xs = self.cache.append_attend(t, qs, kn, vn, par, self.scale)
+        else:
+            self.cache.append(t, kn, vn, par)
+            xs = self.cache.attend(t, qs, self.scale)
         rec = dict(qc=qc, qs=qs, kn=kn, vn=vn, xc=xc, xs=xs,
                    table=self.cache.table(t).clone())
         self.steps.append(rec)
@@ -134,22 +138,24 @@ def _sampled_check(dec, rng):
         assert torch.equal(dec.cache.k_pool[t], rec["kn"]) and torch.equal(dec.cache.v_pool[t], rec["vn"])
 
 
+@pytest.mark.parametrize("fused", [False, True], ids=["split", "fused"])
 @pytest.mark.parametrize("name", ["tiny_fp32", "bf16_b8_m256", "bf16_b32_m1024"])
-def test_workload_full_parity(gpu, name):
+def test_workload_full_parity(gpu, name, fused):
     wl = W.WORKLOADS[name]
-    _log(f"[parity full] {name} seed=0")
-    dec = Decode(wl, 0, gpu)
+    _log(f"[parity full] {name} seed=0 fused={fused}")
+    dec = Decode(wl, 0, gpu, fused)
     for t in range(wl.steps):
         dec.run_step(t)
     torch.cuda.synchronize()
     _full_check(dec)
 
 
+@pytest.mark.parametrize("fused", [False, True], ids=["split", "fused"])
 @pytest.mark.parametrize("name", ["bf16_b64_m4096", "bf16_ragged_b128_m2048"])
-def test_workload_sampled_parity(gpu, name):
+def test_workload_sampled_parity(gpu, name, fused):
     wl = W.WORKLOADS[name]
-    _log(f"[parity sampled] {name} seed=0")
-    dec = Decode(wl, 0, gpu)
+    _log(f"[parity sampled] {name} seed=0 fused={fused}")
+    dec = Decode(wl, 0, gpu, fused)
     for t in range(wl.steps):
         dec.run_step(t)
     torch.cuda.synchronize()
@@ -174,13 +180,14 @@ EDGE = [
 ]
 
 
+@pytest.mark.parametrize("fused", [False, True], ids=["split", "fused"])
 @pytest.mark.parametrize("i", range(len(EDGE)))
-def test_edge_shapes_full_parity(gpu, i):
+def test_edge_shapes_full_parity(gpu, i, fused):
     kw = dict(EDGE[i])
     kw.setdefault("parents", "uniform")
     wl = W.custom(name=f"edge{i}", **kw)
-    _log(f"[parity edge] {wl}")
-    dec = Decode(wl, 1 + i, gpu)
+    _log(f"[parity edge] {wl} fused={fused}")
+    dec = Decode(wl, 1 + i, gpu, fused)
     for t in range(wl.steps):
         dec.run_step(t)
     torch.cuda.synchronize()
@@ -287,3 +294,62 @@ def test_empty_batch_is_noop(gpu):
     off = torch.zeros(1, dtype=torch.int32, device=gpu)
     out = G.grace_cross_attn(q, kv, kv, off, 0)
     assert out.shape == (0, 2, 64)
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 64), ("bf16", 128), ("f32", 32), ("bf16", 32)])
+def test_fused_equals_split_bitwise(gpu, dtype, d):
+    """The fused pass reads the same bits and runs the same arithmetic as append
+    followed by attend: outputs, tables and pools are identical."""
+    wl = W.custom(dtype=dtype, B=3, M=37, H=5, d=d, steps=6, L=20, parents="zipf", zipf_s=1.3)
+    a, b = Decode(wl, 11, gpu, fused=False), Decode(wl, 11, gpu, fused=True)
+    for t in range(wl.steps):
+        ra, rb = a.run_step(t), b.run_step(t)
+        torch.cuda.synchronize()
+        assert torch.equal(ra["xs"], rb["xs"]), f"out t={t}"
+        assert torch.equal(ra["table"][:, :t + 1], rb["table"][:, :t + 1]), f"table t={t}"
+    assert torch.equal(a.cache.k_pool, b.cache.k_pool) and torch.equal(a.cache.v_pool, b.cache.v_pool)
+
+
+def test_fused_aliased_slab(gpu):
+    """Fused call with k_new/v_new already in their slab: no copy, same results."""
+    wl = W.custom(dtype="bf16", B=2, M=48, H=4, d=64, steps=3, L=16)
+    a = Decode(wl, 7, gpu)
+    for t in range(wl.steps):
+        a.run_step(t)
+    cache = G.KVCache(wl.B, wl.M, wl.H, wl.d, wl.steps, wl.torch_dtype, gpu)
+    for t in range(wl.steps):
+        ks, vs = cache.slab(t)
+        ks.copy_(a.inp.step_tensor("k_new", t))
+        vs.copy_(a.inp.step_tensor("v_new", t))
+        par = None if t == 0 else torch.from_numpy(a.parents[t]).to(gpu)
+        out = cache.append_attend(t, a.inp.step_tensor("q_self", t), ks, vs, par)
+        torch.cuda.synchronize()
+        assert torch.equal(out, a.steps[t]["xs"])
+        assert torch.equal(cache.table(t)[:, :t + 1], a.steps[t]["table"][:, :t + 1])
+
+
+def test_fused_out_of_range_parent_sets_flag(gpu):
+    wl = W.custom(dtype="bf16", B=2, M=8, H=2, d=64, steps=2, L=4)   # rows of 256 B
+    dec = Decode(wl, 8, gpu, fused=True)
+    dec.run_step(0)
+    torch.cuda.synchronize()
+    assert int(dec.cache.err_flag.item()) == 0
+    dec.parents[1] = dec.parents[1].copy()
+    dec.parents[1][3] = -2
+    dec.parents[1][12] = wl.M
+    dec.run_step(1)
+    torch.cuda.synchronize()
+    assert int(dec.cache.err_flag.item()) == 1
+    tab = dec.steps[1]["table"].cpu().numpy()
+    assert tab[3, 0] == 0 and tab[12, 0] == 2 * wl.M - 1
+
+
+def test_fused_wave_uniform_rows(gpu):
+    """Rows of exactly 1 KiB and 2 KiB take the wave-uniform (scalar table read) path."""
+    for H, d in ((8, 64), (8, 128)):
+        wl = W.custom(dtype="bf16", B=2, M=33, H=H, d=d, steps=5, L=8, parents="zipf", zipf_s=1.1)
+        dec = Decode(wl, 12, gpu, fused=True)
+        for t in range(wl.steps):
+            dec.run_step(t)
+        torch.cuda.synchronize()
+        _full_check(dec)
