@@ -10,65 +10,45 @@ namespace grace {
 
 // ---------------------------------------------------------------------------
 // kv_append: new block-table rows from the parents' rows, fresh block for the
-// current position, current token copied into its slab.
+// current position, current token copied into its slab.  One 16-byte chunk of
+// the slab per lane (lane g: row g / chunks_per_row, column g % chunks_per_row);
+// the lanes of a row also write its step+1 table entries.  The copy streams
+// past the caches (nontemporal loads and stores): nothing reads it again soon.
 // ---------------------------------------------------------------------------
 
 constexpr int kAppendThreads = 256;
-constexpr int kAppendUnroll = 4;  // 16-byte chunks in flight per thread and tensor
 
 __global__ void __launch_bounds__(kAppendThreads)
 kv_append_kernel(u32x4* __restrict__ k_slab, u32x4* __restrict__ v_slab,
                  const int32_t* __restrict__ table_prev, int32_t* __restrict__ table_next,
                  const int32_t* __restrict__ parents, const u32x4* __restrict__ k_new,
-                 const u32x4* __restrict__ v_new, int32_t R, int32_t M, int32_t T_max,
-                 int32_t step, int32_t rows_per_block, int32_t chunks_per_row, int32_t copy_k,
+                 const u32x4* __restrict__ v_new, int64_t total_chunks, int32_t chunks_per_row,
+                 int32_t R, int32_t M, int32_t T_max, int32_t step, int32_t copy_k,
                  int32_t copy_v, int32_t* __restrict__ err_flag) {
-  const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
-  const int32_t nrows = (int32_t)min<int64_t>(rows_per_block, R - r0);
-  if (nrows <= 0) return;
-
-  // Table: nrows * (step+1) entries.
-  const int32_t cols = step + 1;
-  for (int32_t e = threadIdx.x; e < nrows * cols; e += kAppendThreads) {
-    const int32_t i = (int32_t)r0 + e / cols;
-    const int32_t j = e % cols;
-    int32_t id;
-    if (j == step) {
-      id = step * R + i;
-    } else {
-      int32_t p = parents[i];
+  const int64_t g = (int64_t)blockIdx.x * kAppendThreads + threadIdx.x;
+  if (g >= total_chunks) return;
+  u32x4 kb, vb;
+  if (copy_k) kb = __builtin_nontemporal_load(&k_new[g]);
+  if (copy_v) vb = __builtin_nontemporal_load(&v_new[g]);
+  const int32_t r = (int32_t)(g / chunks_per_row);
+  const int32_t c = (int32_t)(g - (int64_t)r * chunks_per_row);
+  if (c <= step) {
+    int64_t src = 0;
+    if (step > 0) {
+      int32_t p = parents[r];
       if (p < 0 || p >= M) {
         if (err_flag) *err_flag = 1;
         p = p < 0 ? 0 : M - 1;
       }
-      const int32_t src = (i / M) * M + p;
-      id = table_prev[(int64_t)src * T_max + j];
+      src = (int64_t)(r / M) * M + p;
     }
-    table_next[(int64_t)i * T_max + j] = id;
-  }
-
-  // Slab copy: the rows are contiguous in both source and destination.
-  const int64_t base = r0 * chunks_per_row;
-  const int64_t n = (int64_t)nrows * chunks_per_row;
-  for (int64_t c0 = threadIdx.x; c0 < n; c0 += (int64_t)kAppendThreads * kAppendUnroll) {
-    u32x4 kb[kAppendUnroll], vb[kAppendUnroll];
-#pragma unroll
-    for (int u = 0; u < kAppendUnroll; ++u) {
-      const int64_t c = c0 + (int64_t)u * kAppendThreads;
-      if (c < n) {
-        if (copy_k) kb[u] = k_new[base + c];
-        if (copy_v) vb[u] = v_new[base + c];
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < kAppendUnroll; ++u) {
-      const int64_t c = c0 + (int64_t)u * kAppendThreads;
-      if (c < n) {
-        if (copy_k) k_slab[base + c] = kb[u];
-        if (copy_v) v_slab[base + c] = vb[u];
-      }
+    for (int32_t j = c; j <= step; j += chunks_per_row) {
+      const int32_t id = j == step ? step * R + r : table_prev[src * T_max + j];
+      table_next[(int64_t)r * T_max + j] = id;
     }
   }
+  if (copy_k) __builtin_nontemporal_store(kb, &k_slab[g]);
+  if (copy_v) __builtin_nontemporal_store(vb, &v_slab[g]);
 }
 
 hipError_t launch_kv_append(void* k_slab, void* v_slab, const int32_t* table_prev,
@@ -77,15 +57,12 @@ hipError_t launch_kv_append(void* k_slab, void* v_slab, const int32_t* table_pre
                             int32_t row_bytes, bool copy_k, bool copy_v, int32_t* err_flag,
                             hipStream_t stream) {
   const int32_t chunks_per_row = row_bytes / 16;
-  // About 32 KiB of each tensor per block.
-  int32_t rows_per_block = (32 * 1024) / row_bytes;
-  if (rows_per_block < 1) rows_per_block = 1;
-  if (rows_per_block > 256) rows_per_block = 256;
-  const int64_t blocks = ((int64_t)R + rows_per_block - 1) / rows_per_block;
+  const int64_t total = (int64_t)R * chunks_per_row;
+  const int64_t blocks = (total + kAppendThreads - 1) / kAppendThreads;
   hipLaunchKernelGGL(kv_append_kernel, dim3((unsigned)blocks), dim3(kAppendThreads), 0, stream,
                      (u32x4*)k_slab, (u32x4*)v_slab, table_prev, table_next, parents,
-                     (const u32x4*)k_new, (const u32x4*)v_new, R, M, T_max, step, rows_per_block,
-                     chunks_per_row, (int32_t)copy_k, (int32_t)copy_v, err_flag);
+                     (const u32x4*)k_new, (const u32x4*)v_new, total, chunks_per_row, R, M, T_max,
+                     step, (int32_t)copy_k, (int32_t)copy_v, err_flag);
   return hipGetLastError();
 }
 
@@ -96,7 +73,10 @@ hipError_t launch_kv_append(void* k_slab, void* v_slab, const int32_t* table_pre
 // consecutive chunks and is owned by CH consecutive lanes (CH divides 64, so a
 // head never straddles two waves).  Lane group sums give the scores, every
 // lane of the group keeps all NT scores, and the softmax over NT <= 8 values
-// runs in registers.  Each lane issues all of its q/K/V loads before any math.
+// runs in registers.  One chunk per lane; each lane issues all of its q/K/V
+// loads before any math.  Streams read or written once (q, the current token,
+// the slab written, out) bypass the caches; ancestor blocks, which sibling
+// beams share, are ordinary cached loads.
 // When a row is a whole number of waves (H*d*elem a multiple of 1 KiB), the
 // row index is wave-uniform and the table/parent reads become scalar loads.
 // ---------------------------------------------------------------------------
@@ -158,46 +138,34 @@ __device__ __forceinline__ int64_t row_of(int64_t g, int32_t chunks_per_row) {
   return r;
 }
 
-template <class T, int D, int NT, int U, bool UNIFORM>
+template <class T, int D, int NT, bool UNIFORM>
 __global__ void __launch_bounds__(kSelfThreads)
 self_attn_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_pool,
                  const u32x4* __restrict__ v_pool, const int32_t* __restrict__ table,
                  u32x4* __restrict__ out, int64_t total_chunks, int32_t chunks_per_row,
                  int32_t T_max, uint32_t nblocks, float c_scale) {
-  const int64_t first = ((int64_t)blockIdx.x * kSelfThreads + threadIdx.x);
-  const int64_t stride_u = (int64_t)gridDim.x * kSelfThreads;
-
-  u32x4 qc[U], kc[U][NT], vc[U][NT];
-  bool live[U];
+  const int64_t g = (int64_t)blockIdx.x * kSelfThreads + threadIdx.x;
+  if (g >= total_chunks) return;   // wave-uniform when UNIFORM (rows are whole waves)
+  const int64_t r = row_of<UNIFORM>(g, chunks_per_row);
+  const int32_t c = (int32_t)(g - r * chunks_per_row);
+  u32x4 kc[NT], vc[NT];
+  const u32x4 qc = __builtin_nontemporal_load(&q[g]);
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int64_t g = first + u * stride_u;
-    live[u] = g < total_chunks;
-    const int64_t gg = live[u] ? g : 0;
-    const int64_t r = row_of<UNIFORM>(gg, chunks_per_row);
-    const int32_t c = (int32_t)(gg - r * chunks_per_row);
-    qc[u] = __builtin_nontemporal_load(&q[gg]);
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      uint32_t id = (uint32_t)table[r * T_max + j];
-      id = id < nblocks ? id : nblocks - 1;
-      const int64_t off = (int64_t)id * chunks_per_row + c;
-      kc[u][j] = k_pool[off];
-      vc[u][j] = v_pool[off];
-    }
+  for (int j = 0; j < NT; ++j) {
+    uint32_t id = (uint32_t)table[r * T_max + j];
+    id = id < nblocks ? id : nblocks - 1;
+    const int64_t off = (int64_t)id * chunks_per_row + c;
+    kc[j] = k_pool[off];
+    vc[j] = v_pool[off];
   }
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const u32x4 o = attend_chunk<T, D, NT>(qc[u], kc[u], vc[u], c_scale);
-    if (live[u]) __builtin_nontemporal_store(o, &out[first + u * stride_u]);
-  }
+  __builtin_nontemporal_store(attend_chunk<T, D, NT>(qc, kc, vc, c_scale), &out[g]);
 }
 
 // Fused append + attend (the paper's fused and paged self-attention): each row
 // takes its parent's block ids for positions < step, writes them and its fresh
 // block id to table_next, stores the current token's k/v into slab `step`, and
 // attends over the ancestors' blocks plus the current token held in registers.
-template <class T, int D, int NT, int U, bool UNIFORM>
+template <class T, int D, int NT, bool UNIFORM>
 __global__ void __launch_bounds__(kSelfThreads)
 self_attn_fused_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_new,
                        const u32x4* __restrict__ v_new, u32x4* __restrict__ k_pool,
@@ -207,67 +175,47 @@ self_attn_fused_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_
                        int32_t R, int32_t M, int32_t T_max, uint32_t nblocks, float c_scale,
                        int32_t copy_k, int32_t copy_v, int32_t* __restrict__ err_flag) {
   constexpr int STEP = NT - 1;
-  const int64_t first = ((int64_t)blockIdx.x * kSelfThreads + threadIdx.x);
-  const int64_t stride_u = (int64_t)gridDim.x * kSelfThreads;
-  const int64_t slab = (int64_t)STEP * R * chunks_per_row;   // chunk offset of slab `step`
+  const int64_t g = (int64_t)blockIdx.x * kSelfThreads + threadIdx.x;
+  if (g >= total_chunks) return;   // wave-uniform when UNIFORM (rows are whole waves)
+  const int64_t r = row_of<UNIFORM>(g, chunks_per_row);
+  const int32_t c = (int32_t)(g - r * chunks_per_row);
 
-  u32x4 qc[U], kc[U][NT], vc[U][NT];
-  int32_t ids[U][NT > 1 ? NT - 1 : 1];
-  int64_t rows[U];
-  int32_t cols[U];
-  bool live[U];
+  u32x4 kc[NT], vc[NT];
+  int32_t ids[NT > 1 ? NT - 1 : 1];
+  const u32x4 qc = __builtin_nontemporal_load(&q[g]);
+  kc[STEP] = __builtin_nontemporal_load(&k_new[g]);
+  vc[STEP] = __builtin_nontemporal_load(&v_new[g]);
+  if constexpr (STEP > 0) {
+    int32_t p = parents[r];
+    if (p < 0 || p >= M) {
+      if (err_flag) *err_flag = 1;
+      p = p < 0 ? 0 : M - 1;
+    }
+    const int64_t src = (r / M) * M + p;
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int64_t g = first + u * stride_u;
-    live[u] = g < total_chunks;
-    const int64_t gg = live[u] ? g : 0;
-    const int64_t r = row_of<UNIFORM>(gg, chunks_per_row);
-    const int32_t c = (int32_t)(gg - r * chunks_per_row);
-    rows[u] = r;
-    cols[u] = c;
-    qc[u] = __builtin_nontemporal_load(&q[gg]);
-    kc[u][STEP] = __builtin_nontemporal_load(&k_new[gg]);
-    vc[u][STEP] = __builtin_nontemporal_load(&v_new[gg]);
-    if constexpr (STEP > 0) {
-      int32_t p = parents[r];
-      if (p < 0 || p >= M) {
-        if (live[u] && err_flag) *err_flag = 1;
-        p = p < 0 ? 0 : M - 1;
-      }
-      const int64_t src = (r / M) * M + p;
-#pragma unroll
-      for (int j = 0; j < STEP; ++j) {
-        uint32_t id = (uint32_t)table_prev[src * T_max + j];
-        ids[u][j] = (int32_t)id;
-        id = id < nblocks ? id : nblocks - 1;
-        const int64_t off = (int64_t)id * chunks_per_row + c;
-        kc[u][j] = k_pool[off];
-        vc[u][j] = v_pool[off];
-      }
+    for (int j = 0; j < STEP; ++j) {
+      uint32_t id = (uint32_t)table_prev[src * T_max + j];
+      ids[j] = (int32_t)id;
+      id = id < nblocks ? id : nblocks - 1;
+      const int64_t off = (int64_t)id * chunks_per_row + c;
+      kc[j] = k_pool[off];
+      vc[j] = v_pool[off];
     }
   }
+
+  // Append: slab `step` (streamed past the caches) and the row's table entries.
+  const int64_t slab = (int64_t)STEP * R * chunks_per_row;
+  if (copy_k) __builtin_nontemporal_store(kc[STEP], &k_pool[slab + g]);
+  if (copy_v) __builtin_nontemporal_store(vc[STEP], &v_pool[slab + g]);
+  for (int32_t j = c; j <= STEP; j += chunks_per_row) {
+    int32_t id = (int32_t)(STEP * R + r);
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    if (!live[u]) continue;
-    const int64_t g = first + u * stride_u;
-    if (copy_k) k_pool[slab + g] = kc[u][STEP];
-    if (copy_v) v_pool[slab + g] = vc[u][STEP];
-    const int32_t c = cols[u];
-    if (c <= STEP) {
-      int32_t id = (int32_t)(STEP * R + rows[u]);
-      if constexpr (STEP > 0) {
-#pragma unroll
-        for (int j = 0; j < STEP; ++j)
-          if (c == j) id = ids[u][j];
-      }
-      table_next[rows[u] * T_max + c] = id;
-    }
+    for (int i = 0; i < STEP; ++i)
+      if (j == i) id = ids[i];
+    table_next[r * T_max + j] = id;
   }
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const u32x4 o = attend_chunk<T, D, NT>(qc[u], kc[u], vc[u], c_scale);
-    if (live[u]) __builtin_nontemporal_store(o, &out[first + u * stride_u]);
-  }
+
+  __builtin_nontemporal_store(attend_chunk<T, D, NT>(qc, kc, vc, c_scale), &out[g]);
 }
 
 struct SelfArgs {
@@ -290,24 +238,20 @@ struct SelfArgs {
 
 template <bool FUSED, class T, int D, int NT>
 static hipError_t launch_self_nt(const SelfArgs& a, hipStream_t stream) {
-  // Two chunks per lane keep 2*(2*NT+1) 16-byte loads in flight per lane.
-  constexpr int U = NT <= 4 ? 2 : 1;
-  int64_t waves_needed = (a.total_chunks + 64 * U - 1) / (64 * U);
-  int64_t blocks = (waves_needed + (kSelfThreads / 64) - 1) / (kSelfThreads / 64);
-  if (blocks < 1) blocks = 1;
+  const int64_t blocks = (a.total_chunks + kSelfThreads - 1) / kSelfThreads;
   const bool uniform = a.chunks_per_row % 64 == 0;
-#define GRACE_GO(UNI)                                                                               \
-  if constexpr (FUSED) {                                                                           \
-    hipLaunchKernelGGL((self_attn_fused_kernel<T, D, NT, U, UNI>), dim3((unsigned)blocks),         \
-                       dim3(kSelfThreads), 0, stream, (const u32x4*)a.q, (const u32x4*)a.k_new,    \
-                       (const u32x4*)a.v_new, (u32x4*)a.k_pool, (u32x4*)a.v_pool, a.table_prev,    \
-                       a.table_next, a.parents, (u32x4*)a.out, a.total_chunks, a.chunks_per_row,    \
-                       a.R, a.M, a.T_max, a.nblocks, a.c_scale, a.copy_k, a.copy_v, a.err_flag);   \
-  } else {                                                                                         \
-    hipLaunchKernelGGL((self_attn_kernel<T, D, NT, U, UNI>), dim3((unsigned)blocks),               \
-                       dim3(kSelfThreads), 0, stream, (const u32x4*)a.q, (const u32x4*)a.k_pool,   \
-                       (const u32x4*)a.v_pool, a.table_prev, (u32x4*)a.out, a.total_chunks,         \
-                       a.chunks_per_row, a.T_max, a.nblocks, a.c_scale);                           \
+#define GRACE_GO(UNI)                                                                              \
+  if constexpr (FUSED) {                                                                          \
+    hipLaunchKernelGGL((self_attn_fused_kernel<T, D, NT, UNI>), dim3((unsigned)blocks),           \
+                       dim3(kSelfThreads), 0, stream, (const u32x4*)a.q, (const u32x4*)a.k_new,   \
+                       (const u32x4*)a.v_new, (u32x4*)a.k_pool, (u32x4*)a.v_pool, a.table_prev,   \
+                       a.table_next, a.parents, (u32x4*)a.out, a.total_chunks, a.chunks_per_row,   \
+                       a.R, a.M, a.T_max, a.nblocks, a.c_scale, a.copy_k, a.copy_v, a.err_flag);  \
+  } else {                                                                                        \
+    hipLaunchKernelGGL((self_attn_kernel<T, D, NT, UNI>), dim3((unsigned)blocks),                 \
+                       dim3(kSelfThreads), 0, stream, (const u32x4*)a.q, (const u32x4*)a.k_pool,  \
+                       (const u32x4*)a.v_pool, a.table_prev, (u32x4*)a.out, a.total_chunks,        \
+                       a.chunks_per_row, a.T_max, a.nblocks, a.c_scale);                          \
   }
   if (uniform) {
     GRACE_GO(true)
