@@ -13,7 +13,13 @@
  *                         prefix, positions 0..step (Sec. 5.2, Sec. 5.3);
  *   grace_self_attn_step_fused
  *                         the previous two in one pass: table update, append
- *                         and self-attention (Sec. 5.2 kernel fusion, Sec. 5.3).
+ *                         and self-attention (Sec. 5.2 kernel fusion, Sec. 5.3);
+ *                         _dyn: the same with per-step beam widths (Sec. 3.3);
+ *   grace_beam_scores     beam score update: prefix score + token log-prob,
+ *                         filtered tokens removed (Sec. 3.1);
+ *   grace_beam_topk       per-request top-k that yields the next step's beams,
+ *                         i.e. the parents the rearrangement consumes (Sec. 3.1,
+ *                         Sec. 3.3).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -188,6 +194,86 @@ int32_t grace_self_attn_step_fused(const void* q, const void* k_new, const void*
                                    int32_t M, int32_t H, int32_t d, int32_t T_max, int32_t step,
                                    float scale, int32_t dtype, void* out, int32_t* err_flag,
                                    void* stream);
+
+/*
+ * grace_self_attn_step_fused with dynamic per-step beam widths (Sec. 3.3): the
+ * previous step kept M_prev beams per request, this step keeps M_cur, and the
+ * pools reserve R_s rows per slab (R_s >= B*M_cur and >= B*M_prev; slab t holds
+ * the B*M_t rows of step t).  With new row r = b*M_cur + j:
+ *   table_next[r, j'] = table_prev[b*M_prev + parents[r], j']  for 0 <= j' < step
+ *   table_next[r, step] = step*R_s + r
+ *   k_pool[step, r] = k_new[r],  v_pool[step, r] = v_new[r]
+ * and out is the self-attention over table_next[r, 0..step] as in
+ * grace_self_attn_step_fused.  Pools are [T_max, R_s, H, d]; block ids index
+ * them as [T_max*R_s, H, d] and are clamped into that range on the device.
+ *
+ *   q, k_new, v_new, out   device, [B*M_cur, H, d], dtype
+ *   table_prev             device, int32 [B*M_prev, T_max] (read for step > 0)
+ *   table_next             device, int32 [B*M_cur, T_max]
+ *   parents                device, int32 [B*M_cur], request-local parents in [0, M_prev);
+ *                          out-of-range entries are clamped and set *err_flag
+ *   M_prev                 ignored at step 0; else >= 1
+ *   other arguments        as for grace_self_attn_step_fused
+ * Limits: T_max*R_s and R_s*H*d below 2^31.  Aliasing rules as for
+ * grace_self_attn_step_fused (slab `step` means rows step*R_s .. step*R_s+B*M_cur-1).
+ */
+int32_t grace_self_attn_step_fused_dyn(const void* q, const void* k_new, const void* v_new,
+                                       void* k_pool, void* v_pool, const int32_t* table_prev,
+                                       int32_t* table_next, const int32_t* parents, int32_t B,
+                                       int32_t M_prev, int32_t M_cur, int32_t R_s, int32_t H,
+                                       int32_t d, int32_t T_max, int32_t step, float scale,
+                                       int32_t dtype, void* out, int32_t* err_flag, void* stream);
+
+/*
+ * Beam score update (Sec. 3.1): every candidate (beam row r, token v) scores
+ *   cand[r, v] = prev_scores[r] + log_softmax(logits[r, :])[v]      if allowed
+ *   cand[r, v] = -inf                                                if filtered
+ * The log-softmax is over the whole vocabulary (the filter removes candidates
+ * after the model's distribution is formed; no renormalisation over survivors).
+ * Arithmetic in fp32.
+ *
+ *   logits       device, [R, V], dtype (GRACE_F32 or GRACE_BF16)
+ *   prev_scores  device, fp32 [R]; accumulated log-probability of each beam's prefix
+ *   mask         device, uint32 [R, ceil(V/32)] or NULL (all allowed): bit (v % 32)
+ *                of word v / 32 of row r set = token v allowed for beam r (the
+ *                constraint filter's output)
+ *   R, V         rows and vocabulary size; R*V below 2^31, V >= 1
+ *   cand         device, fp32 [R, V], written; must not overlap the inputs
+ *   row_max      device, fp32 [R] or NULL; receives max_v cand[r, v]
+ *   stream       hipStream_t
+ */
+int32_t grace_beam_scores(const void* logits, const float* prev_scores, const uint32_t* mask,
+                          int32_t R, int32_t V, int32_t dtype, float* cand, float* row_max,
+                          void* stream);
+
+/* Largest k grace_beam_topk accepts. */
+int32_t grace_beam_topk_max_k(void);
+
+/*
+ * Per-request beam top-k (Sec. 3.1; with dynamic widths k = M_{t+1}, Sec. 3.3).
+ * Request b owns candidates cand[b*M + m, v], flat index i = m*V + v.  The k
+ * best are selected under a total order: score descending, then flat index
+ * ascending (-0 equals +0; NaN ranks below -inf), and are written in that
+ * order: for j < k,
+ *   parents[b*k + j] = i_j / V   (request-local beam in [0, M): the parent of
+ *                                 new beam j, as grace_kv_append and the fused
+ *                                 entry points consume it with M_cur = k)
+ *   tokens[b*k + j]  = i_j % V,  scores[b*k + j] = cand at i_j (bit-exact)
+ * k beams are always produced; when fewer than k candidates are finite the
+ * rest are filtered candidates (score -inf, dead beams).
+ *
+ *   cand      device, fp32 [B*M, V]
+ *   row_max   device, fp32 [B*M] or NULL: a speed hint (grace_beam_scores'
+ *             row maxima); any values give the same result
+ *   B, M, V   requests, beams per request, vocabulary; M*V below 2^31
+ *   k         1 <= k <= min(M*V, grace_beam_topk_max_k())
+ *   parents, tokens   device, int32 [B, k];  scores  device, fp32 [B, k]
+ *   stream    hipStream_t
+ * Outputs must not overlap each other or the inputs.
+ */
+int32_t grace_beam_topk(const float* cand, const float* row_max, int32_t B, int32_t M, int32_t V,
+                        int32_t k, int32_t* parents, int32_t* tokens, float* scores,
+                        void* stream);
 
 /* Human-readable name of a status code (static storage; never NULL). */
 const char* grace_status_string(int32_t status);

@@ -137,42 +137,51 @@ int32_t grace_self_attn_step(const void* q, const void* k_pool, const void* v_po
                                                  (hipStream_t)stream));
 }
 
-int32_t grace_self_attn_step_fused(const void* q, const void* k_new, const void* v_new,
-                                   void* k_pool, void* v_pool, const int32_t* table_prev,
-                                   int32_t* table_next, const int32_t* parents, int32_t B,
-                                   int32_t M, int32_t H, int32_t d, int32_t T_max, int32_t step,
-                                   float scale, int32_t dtype, void* out, int32_t* err_flag,
-                                   void* stream) {
+}  // extern "C"
+
+namespace {
+
+struct Range {
+  const void* p;
+  int64_t n;
+};
+
+// Shared by the fixed- and dynamic-width fused entry points: R = B*M_cur rows
+// written this step, parents index B*M_prev previous rows, slab row stride R_s.
+int32_t fused_impl(const void* q, const void* k_new, const void* v_new, void* k_pool,
+                   void* v_pool, const int32_t* table_prev, int32_t* table_next,
+                   const int32_t* parents, int32_t B, int32_t M_prev, int32_t M_cur, int32_t R_s,
+                   int32_t H, int32_t d, int32_t T_max, int32_t step, float scale, int32_t dtype,
+                   void* out, int32_t* err_flag, void* stream) {
   int64_t R, row_bytes;
-  int32_t st = check_shape(B, M, H, d, dtype, R, row_bytes);
+  int32_t st = check_shape(B, M_cur, H, d, dtype, R, row_bytes);
   if (st != GRACE_OK) return st;
   if (T_max < 1 || T_max > 8 || step < 0 || step >= T_max) return GRACE_ERR_SHAPE;
-  if ((int64_t)T_max * R >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
   if (!good_scale(scale)) return GRACE_ERR_SHAPE;
   if (R == 0) return GRACE_OK;
+  if (R_s < R || (int64_t)T_max * R_s >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
+  if ((int64_t)R_s * H * d >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
+  if (step > 0 && (M_prev < 1 || (int64_t)B * M_prev > R_s)) return GRACE_ERR_SHAPE;
   if (!q || !k_new || !v_new || !k_pool || !v_pool || !table_next || !out) return GRACE_ERR_NULL;
   if (step > 0 && (!table_prev || !parents)) return GRACE_ERR_NULL;
-  const int64_t slab = R * row_bytes, table_bytes = R * T_max * 4;
-  char* k_slab = (char*)k_pool + step * slab;
-  char* v_slab = (char*)v_pool + step * slab;
+  const int64_t rows_bytes = R * row_bytes, slab_bytes = (int64_t)R_s * row_bytes;
+  char* k_slab = (char*)k_pool + step * slab_bytes;
+  char* v_slab = (char*)v_pool + step * slab_bytes;
   const bool copy_k = k_new != (const void*)k_slab;
   const bool copy_v = v_new != (const void*)v_slab;
-  struct Range {
-    const void* p;
-    int64_t n;
-  };
+  const int64_t prev_table_bytes = step > 0 ? (int64_t)B * M_prev * T_max * 4 : 0;
   // Written ranges, then read ranges.  An uncopied slab is read (as k_new/v_new), not written.
-  const Range writes[4] = {{out, slab},
-                           {table_next, table_bytes},
-                           {copy_k ? k_slab : nullptr, copy_k ? slab : 0},
-                           {copy_v ? v_slab : nullptr, copy_v ? slab : 0}};
-  const Range reads[7] = {{q, slab},
-                          {k_new, slab},
-                          {v_new, slab},
-                          {step > 0 ? table_prev : nullptr, step > 0 ? table_bytes : 0},
+  const Range writes[4] = {{out, rows_bytes},
+                           {table_next, R * T_max * 4},
+                           {copy_k ? k_slab : nullptr, copy_k ? rows_bytes : 0},
+                           {copy_v ? v_slab : nullptr, copy_v ? rows_bytes : 0}};
+  const Range reads[7] = {{q, rows_bytes},
+                          {k_new, rows_bytes},
+                          {v_new, rows_bytes},
+                          {step > 0 ? table_prev : nullptr, prev_table_bytes},
                           {step > 0 ? parents : nullptr, step > 0 ? R * 4 : 0},
-                          {k_pool, step * slab},
-                          {v_pool, step * slab}};
+                          {k_pool, step * slab_bytes},
+                          {v_pool, step * slab_bytes}};
   for (int i = 0; i < 4; ++i) {
     for (int j = i + 1; j < 4; ++j)
       if (overlaps(writes[i].p, writes[i].n, writes[j].p, writes[j].n)) return GRACE_ERR_ALIAS;
@@ -180,8 +189,76 @@ int32_t grace_self_attn_step_fused(const void* q, const void* k_new, const void*
       if (overlaps(writes[i].p, writes[i].n, reads[j].p, reads[j].n)) return GRACE_ERR_ALIAS;
   }
   return hip_status(grace::launch_self_attn_fused(
-      q, k_new, v_new, k_pool, v_pool, table_prev, table_next, parents, out, (int32_t)R, M, H, d,
-      T_max, step, scale, dtype == GRACE_BF16, copy_k, copy_v, err_flag, (hipStream_t)stream));
+      q, k_new, v_new, k_pool, v_pool, table_prev, table_next, parents, out, (int32_t)R, M_cur,
+      M_prev, R_s, H, d, T_max, step, scale, dtype == GRACE_BF16, copy_k, copy_v, err_flag,
+      (hipStream_t)stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t grace_self_attn_step_fused(const void* q, const void* k_new, const void* v_new,
+                                   void* k_pool, void* v_pool, const int32_t* table_prev,
+                                   int32_t* table_next, const int32_t* parents, int32_t B,
+                                   int32_t M, int32_t H, int32_t d, int32_t T_max, int32_t step,
+                                   float scale, int32_t dtype, void* out, int32_t* err_flag,
+                                   void* stream) {
+  if (B < 0 || M < 0 || (int64_t)B * M >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
+  return fused_impl(q, k_new, v_new, k_pool, v_pool, table_prev, table_next, parents, B, M, M,
+                    B * M, H, d, T_max, step, scale, dtype, out, err_flag, stream);
+}
+
+int32_t grace_self_attn_step_fused_dyn(const void* q, const void* k_new, const void* v_new,
+                                       void* k_pool, void* v_pool, const int32_t* table_prev,
+                                       int32_t* table_next, const int32_t* parents, int32_t B,
+                                       int32_t M_prev, int32_t M_cur, int32_t R_s, int32_t H,
+                                       int32_t d, int32_t T_max, int32_t step, float scale,
+                                       int32_t dtype, void* out, int32_t* err_flag,
+                                       void* stream) {
+  return fused_impl(q, k_new, v_new, k_pool, v_pool, table_prev, table_next, parents, B, M_prev,
+                    M_cur, R_s, H, d, T_max, step, scale, dtype, out, err_flag, stream);
+}
+
+int32_t grace_beam_scores(const void* logits, const float* prev_scores, const uint32_t* mask,
+                          int32_t R, int32_t V, int32_t dtype, float* cand, float* row_max,
+                          void* stream) {
+  if (dtype != GRACE_F32 && dtype != GRACE_BF16) return GRACE_ERR_UNSUPPORTED;
+  if (R < 0 || V < 1 || (int64_t)R * V >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
+  if (R == 0) return GRACE_OK;
+  if (!logits || !prev_scores || !cand) return GRACE_ERR_NULL;
+  const int64_t n = (int64_t)R * V;
+  const int64_t mask_bytes = mask ? (int64_t)R * ((V + 31) / 32) * 4 : 0;
+  const Range reads[3] = {{logits, n * elem_bytes(dtype)}, {prev_scores, R * 4}, {mask, mask_bytes}};
+  for (const Range& r : reads) {
+    if (overlaps(cand, n * 4, r.p, r.n)) return GRACE_ERR_ALIAS;
+    if (row_max && overlaps(row_max, (int64_t)R * 4, r.p, r.n)) return GRACE_ERR_ALIAS;
+  }
+  if (row_max && overlaps(row_max, (int64_t)R * 4, cand, n * 4)) return GRACE_ERR_ALIAS;
+  return hip_status(grace::launch_beam_scores(logits, prev_scores, mask, cand, row_max, R, V,
+                                              dtype == GRACE_BF16, (hipStream_t)stream));
+}
+
+int32_t grace_beam_topk_max_k(void) { return grace::beam_topk_max_k(); }
+
+int32_t grace_beam_topk(const float* cand, const float* row_max, int32_t B, int32_t M, int32_t V,
+                        int32_t k, int32_t* parents, int32_t* tokens, float* scores,
+                        void* stream) {
+  if (B < 0 || M < 1 || V < 1 || (int64_t)M * V >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
+  if (k < 1 || k > grace::beam_topk_max_k() || (int64_t)k > (int64_t)M * V) return GRACE_ERR_SHAPE;
+  if ((int64_t)B * k >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
+  if (B == 0) return GRACE_OK;
+  if (!cand || !parents || !tokens || !scores) return GRACE_ERR_NULL;
+  const int64_t n = (int64_t)B * M * V * 4, outb = (int64_t)B * k * 4;
+  const Range outs[3] = {{parents, outb}, {tokens, outb}, {scores, outb}};
+  for (int i = 0; i < 3; ++i) {
+    for (int j = i + 1; j < 3; ++j)
+      if (overlaps(outs[i].p, outs[i].n, outs[j].p, outs[j].n)) return GRACE_ERR_ALIAS;
+    if (overlaps(outs[i].p, outs[i].n, cand, n)) return GRACE_ERR_ALIAS;
+    if (row_max && overlaps(outs[i].p, outs[i].n, row_max, (int64_t)B * M * 4)) return GRACE_ERR_ALIAS;
+  }
+  return hip_status(grace::launch_beam_topk(cand, row_max, B, M, V, k, parents, tokens, scores,
+                                            (hipStream_t)stream));
 }
 
 }  // extern "C"

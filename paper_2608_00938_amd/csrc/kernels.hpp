@@ -26,12 +26,24 @@ hipError_t launch_self_attn_step(const void* q, const void* k_pool, const void* 
                                  hipStream_t stream);
 
 // Fused append + attend: table update, slab write (unless aliased) and
-// self-attention over step+1 tokens in one pass.
+// self-attention over step+1 tokens in one pass.  R = B*M rows this step,
+// parents index B*M_prev previous rows, pool slabs have row stride R_s.
 hipError_t launch_self_attn_fused(const void* q, const void* k_new, const void* v_new,
                                   void* k_pool, void* v_pool, const int32_t* table_prev,
                                   int32_t* table_next, const int32_t* parents, void* out, int32_t R,
-                                  int32_t M, int32_t H, int32_t d, int32_t T_max, int32_t step,
-                                  float scale, bool bf16, bool copy_k, bool copy_v,
-                                  int32_t* err_flag, hipStream_t stream);
+                                  int32_t M, int32_t M_prev, int32_t R_s, int32_t H, int32_t d,
+                                  int32_t T_max, int32_t step, float scale, bool bf16, bool copy_k,
+                                  bool copy_v, int32_t* err_flag, hipStream_t stream);
+
+// Beam candidate scores: prev[r] + log_softmax(logits[r]), -inf where filtered.
+hipError_t launch_beam_scores(const void* logits, const float* prev, const uint32_t* mask,
+                              float* cand, float* row_max, int32_t R, int32_t V, bool bf16,
+                              hipStream_t stream);
+
+// Per-request top-k over M*V candidates; k <= beam_topk_max_k().
+hipError_t launch_beam_topk(const float* cand, const float* row_max, int32_t B, int32_t M,
+                            int32_t V, int32_t k, int32_t* parents, int32_t* tokens,
+                            float* scores, hipStream_t stream);
+int32_t beam_topk_max_k();
 
 }  // namespace grace

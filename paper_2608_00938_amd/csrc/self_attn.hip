@@ -172,8 +172,9 @@ self_attn_fused_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_
                        u32x4* __restrict__ v_pool, const int32_t* __restrict__ table_prev,
                        int32_t* __restrict__ table_next, const int32_t* __restrict__ parents,
                        u32x4* __restrict__ out, int64_t total_chunks, int32_t chunks_per_row,
-                       int32_t R, int32_t M, int32_t T_max, uint32_t nblocks, float c_scale,
-                       int32_t copy_k, int32_t copy_v, int32_t* __restrict__ err_flag) {
+                       int32_t R_s, int32_t M, int32_t M_prev, int32_t T_max, uint32_t nblocks,
+                       float c_scale, int32_t copy_k, int32_t copy_v,
+                       int32_t* __restrict__ err_flag) {
   constexpr int STEP = NT - 1;
   const int64_t g = (int64_t)blockIdx.x * kSelfThreads + threadIdx.x;
   if (g >= total_chunks) return;   // wave-uniform when UNIFORM (rows are whole waves)
@@ -187,11 +188,11 @@ self_attn_fused_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_
   vc[STEP] = __builtin_nontemporal_load(&v_new[g]);
   if constexpr (STEP > 0) {
     int32_t p = parents[r];
-    if (p < 0 || p >= M) {
+    if (p < 0 || p >= M_prev) {
       if (err_flag) *err_flag = 1;
-      p = p < 0 ? 0 : M - 1;
+      p = p < 0 ? 0 : M_prev - 1;
     }
-    const int64_t src = (r / M) * M + p;
+    const int64_t src = (r / M) * M_prev + p;   // the parent's row among B*M_prev
 #pragma unroll
     for (int j = 0; j < STEP; ++j) {
       uint32_t id = (uint32_t)table_prev[src * T_max + j];
@@ -204,11 +205,11 @@ self_attn_fused_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_
   }
 
   // Append: slab `step` (streamed past the caches) and the row's table entries.
-  const int64_t slab = (int64_t)STEP * R * chunks_per_row;
+  const int64_t slab = (int64_t)STEP * R_s * chunks_per_row;
   if (copy_k) __builtin_nontemporal_store(kc[STEP], &k_pool[slab + g]);
   if (copy_v) __builtin_nontemporal_store(vc[STEP], &v_pool[slab + g]);
   for (int32_t j = c; j <= STEP; j += chunks_per_row) {
-    int32_t id = (int32_t)(STEP * R + r);
+    int32_t id = (int32_t)(STEP * R_s + r);
 #pragma unroll
     for (int i = 0; i < STEP; ++i)
       if (j == i) id = ids[i];
@@ -229,7 +230,7 @@ struct SelfArgs {
   const int32_t* parents;
   void* out;
   int64_t total_chunks;
-  int32_t chunks_per_row, R, M, T_max;
+  int32_t chunks_per_row, R, M, M_prev, T_max;
   uint32_t nblocks;
   float c_scale;
   int32_t copy_k, copy_v;
@@ -246,7 +247,8 @@ static hipError_t launch_self_nt(const SelfArgs& a, hipStream_t stream) {
                        dim3(kSelfThreads), 0, stream, (const u32x4*)a.q, (const u32x4*)a.k_new,   \
                        (const u32x4*)a.v_new, (u32x4*)a.k_pool, (u32x4*)a.v_pool, a.table_prev,   \
                        a.table_next, a.parents, (u32x4*)a.out, a.total_chunks, a.chunks_per_row,   \
-                       a.R, a.M, a.T_max, a.nblocks, a.c_scale, a.copy_k, a.copy_v, a.err_flag);  \
+                       a.R, a.M, a.M_prev, a.T_max, a.nblocks, a.c_scale, a.copy_k, a.copy_v,      \
+                       a.err_flag);                                                                \
   } else {                                                                                        \
     hipLaunchKernelGGL((self_attn_kernel<T, D, NT, UNI>), dim3((unsigned)blocks),                 \
                        dim3(kSelfThreads), 0, stream, (const u32x4*)a.q, (const u32x4*)a.k_pool,  \
@@ -313,9 +315,9 @@ hipError_t launch_self_attn_step(const void* q, const void* k_pool, const void* 
 hipError_t launch_self_attn_fused(const void* q, const void* k_new, const void* v_new,
                                   void* k_pool, void* v_pool, const int32_t* table_prev,
                                   int32_t* table_next, const int32_t* parents, void* out, int32_t R,
-                                  int32_t M, int32_t H, int32_t d, int32_t T_max, int32_t step,
-                                  float scale, bool bf16, bool copy_k, bool copy_v,
-                                  int32_t* err_flag, hipStream_t stream) {
+                                  int32_t M, int32_t M_prev, int32_t R_s, int32_t H, int32_t d,
+                                  int32_t T_max, int32_t step, float scale, bool bf16, bool copy_k,
+                                  bool copy_v, int32_t* err_flag, hipStream_t stream) {
   SelfArgs a = {};
   const int32_t elem = bf16 ? 2 : 4;
   a.q = q;
@@ -328,11 +330,12 @@ hipError_t launch_self_attn_fused(const void* q, const void* k_new, const void* 
   a.parents = parents;
   a.out = out;
   a.chunks_per_row = H * d * elem / 16;
-  a.total_chunks = (int64_t)R * a.chunks_per_row;
-  a.R = R;
+  a.total_chunks = (int64_t)R * a.chunks_per_row;   // R = B*M rows written this step
+  a.R = R_s;                                        // slab row stride of the pools
   a.M = M;
+  a.M_prev = M_prev;
   a.T_max = T_max;
-  a.nblocks = (uint32_t)((int64_t)T_max * R);
+  a.nblocks = (uint32_t)((int64_t)T_max * R_s);
   a.c_scale = scale * kLog2e;
   a.copy_k = copy_k;
   a.copy_v = copy_v;

@@ -35,6 +35,15 @@ _SIGNATURES = {
                                    _c_void_p, _c_void_p, _c_void_p, _c_int, _c_int, _c_int,
                                    _c_int, _c_int, _c_int, _c_float, _c_int, _c_void_p, _c_void_p,
                                    _c_void_p],
+    "grace_self_attn_step_fused_dyn": [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+                                       _c_void_p, _c_void_p, _c_void_p, _c_int, _c_int, _c_int,
+                                       _c_int, _c_int, _c_int, _c_int, _c_int, _c_float, _c_int,
+                                       _c_void_p, _c_void_p, _c_void_p],
+    "grace_beam_scores": [_c_void_p, _c_void_p, _c_void_p, _c_int, _c_int, _c_int, _c_void_p,
+                          _c_void_p, _c_void_p],
+    "grace_beam_topk_max_k": [],
+    "grace_beam_topk": [_c_void_p, _c_void_p, _c_int, _c_int, _c_int, _c_int, _c_void_p,
+                        _c_void_p, _c_void_p, _c_void_p],
     "grace_status_string": [_c_int],
     "grace_last_hip_error": [],
     "grace_abi_version": [],
@@ -155,6 +164,65 @@ def grace_self_attn_step_fused(q, k_new, v_new, k_pool, v_pool, table_prev, tabl
     return out
 
 
+def grace_self_attn_step_fused_dyn(q, k_new, v_new, k_pool, v_pool, table_prev, table_next,
+                                   parents, B: int, M_prev: int, M_cur: int, step: int,
+                                   scale: float | None = None, out=None, err_flag=None):
+    """Fused append + attend with per-step beam widths: q/k_new/v_new [B*M_cur, H, d];
+    pools [T_max, R_s, H, d]; tables int32 [>= rows, T_max]; parents int32 [B*M_cur]
+    in [0, M_prev).  Returns out [B*M_cur, H, d]."""
+    _contig(q, k_new, v_new, k_pool, v_pool, table_prev, table_next, parents, out)
+    T_max, R_s, H, d = k_pool.shape
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    if out is None:
+        out = torch.empty_like(q)
+    st = library().grace_self_attn_step_fused_dyn(
+        _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_pool), _ptr(v_pool), _ptr(table_prev),
+        _ptr(table_next), _ptr(parents), B, M_prev, M_cur, R_s, H, d, T_max, step, scale,
+        _dtype_code(q), _ptr(out), _ptr(err_flag), _stream(q))
+    _check(st, "grace_self_attn_step_fused_dyn")
+    return out
+
+
+def grace_beam_scores(logits, prev_scores, mask=None, cand=None, row_max=None):
+    """Candidate scores prev + log_softmax(logits), -inf where the packed mask
+    (uint32 words as int32 [R, ceil(V/32)]) clears the bit.  logits [R, V]
+    (fp32 or bf16); prev_scores fp32 [R].  Returns (cand fp32 [R, V], row_max fp32 [R])."""
+    _contig(logits, prev_scores, mask, cand, row_max)
+    R, V = logits.shape
+    if cand is None:
+        cand = torch.empty((R, V), dtype=torch.float32, device=logits.device)
+    if row_max is None:
+        row_max = torch.empty((R,), dtype=torch.float32, device=logits.device)
+    st = library().grace_beam_scores(_ptr(logits), _ptr(prev_scores), _ptr(mask), R, V,
+                                     _dtype_code(logits), _ptr(cand), _ptr(row_max),
+                                     _stream(logits))
+    _check(st, "grace_beam_scores")
+    return cand, row_max
+
+
+def grace_beam_topk_max_k() -> int:
+    return library().grace_beam_topk_max_k()
+
+
+def grace_beam_topk(cand, B: int, M: int, k: int, row_max=None, parents=None, tokens=None,
+                    scores=None):
+    """Per-request top-k over cand [B*M, V] fp32.  Returns (parents, tokens, scores),
+    each [B, k] (int32, int32, fp32), best first."""
+    _contig(cand, row_max, parents, tokens, scores)
+    V = cand.shape[1]
+    dev = cand.device
+    if parents is None:
+        parents = torch.empty((B, k), dtype=torch.int32, device=dev)
+    if tokens is None:
+        tokens = torch.empty((B, k), dtype=torch.int32, device=dev)
+    if scores is None:
+        scores = torch.empty((B, k), dtype=torch.float32, device=dev)
+    st = library().grace_beam_topk(_ptr(cand), _ptr(row_max), B, M, V, k, _ptr(parents),
+                                   _ptr(tokens), _ptr(scores), _stream(cand))
+    _check(st, "grace_beam_topk")
+    return parents, tokens, scores
+
+
 class KVCache:
     """Caller-side storage of the paged self-attention cache: the two pools and
     a pair of block tables used alternately (the update reads one, writes the
@@ -162,6 +230,7 @@ class KVCache:
 
     def __init__(self, B: int, M: int, H: int, d: int, T_max: int, dtype: torch.dtype,
                  device="cuda"):
+        """M is the beam width (the largest width when steps use dynamic widths)."""
         self.B, self.M, self.H, self.d, self.T_max = B, M, H, d, T_max
         R = B * M
         self.k_pool = torch.empty((T_max, R, H, d), dtype=dtype, device=device)
@@ -184,6 +253,16 @@ class KVCache:
     def attend(self, step: int, q, scale: float | None = None, out=None):
         return grace_self_attn_step(q, self.k_pool, self.v_pool, self.table(step), self.B, self.M,
                                     step, scale=scale, out=out)
+
+    def append_attend_dyn(self, step: int, q, k_new, v_new, parents, M_prev: int, M_cur: int,
+                          scale: float | None = None, out=None):
+        """Fused append + attend at widths M_prev -> M_cur (<= M); slab rows stride B*M."""
+        R = self.B * M_cur
+        return grace_self_attn_step_fused_dyn(q, k_new, v_new, self.k_pool, self.v_pool,
+                                              self.tables[(step + 1) % 2],
+                                              self.tables[step % 2][:R], parents, self.B,
+                                              M_prev, M_cur, step, scale=scale, out=out,
+                                              err_flag=self.err_flag)
 
     def append_attend(self, step: int, q, k_new, v_new, parents=None, scale: float | None = None,
                       out=None):

@@ -29,12 +29,19 @@ import torch
 
 F32 = "f32"
 BF16 = "bf16"
+TORCH_DTYPES = {F32: torch.float32, BF16: torch.bfloat16}
 
 _TORCH_DTYPE = {F32: torch.float32, BF16: torch.bfloat16}
 
 # Tensor tags used in the per-tensor seed.
 _TAG = {"enc_k": 1, "enc_v": 2, "q_cross": 3, "q_self": 4, "k_new": 5, "v_new": 6,
-        "parents": 7, "lengths": 8, "perm": 9}
+        "parents": 7, "lengths": 8, "perm": 9, "logits": 10, "prev_scores": 11, "mask": 12,
+        "cand": 13, "dyn_parents": 14}
+
+# Beam step shapes of the paper's model (Sec. 3.2, Sec. 3.3): SID-token
+# vocabulary and the dynamic per-step beam widths (M_1, ..., M_4).
+VOCAB = 512
+DYN_WIDTHS = (1, 512, 1024, 1024)
 
 
 @dataclass(frozen=True)
@@ -185,3 +192,70 @@ class DecodeInputs:
 
     def parents(self, step: int) -> np.ndarray | None:
         return parents(self.wl, step, self.seed)
+
+
+# ---------------------------------------------------------------------------
+# Beam-step inputs (score update and top-k).  Plain seeded draws: logits
+# N(0, 3^2) (rounded to bf16 when asked), accumulated prefix log-probabilities
+# -Gamma(step + 1, 3), and a filter that keeps each token with probability
+# ``keep`` (packed 32 tokens per uint32 word, bit v % 32 of word v // 32).
+# ---------------------------------------------------------------------------
+
+def beam_logits(seed: int, step: int, R: int, V: int, dtype: str = BF16,
+                device: str | torch.device = "cpu") -> torch.Tensor:
+    x = torch.from_numpy(_rng(seed, "logits", step).standard_normal((R, V)).astype(np.float32) * 3)
+    return x.to(TORCH_DTYPES[dtype]).to(device)
+
+
+def beam_prev_scores(seed: int, step: int, R: int) -> np.ndarray:
+    return (-_rng(seed, "prev_scores", step).gamma(step + 1.0, 3.0, size=R)).astype(np.float32)
+
+
+def beam_mask(seed: int, step: int, R: int, V: int, keep: float = 0.6) -> np.ndarray:
+    """uint32 [R, ceil(V/32)] filter words; bits past V are zero."""
+    allowed = _rng(seed, "mask", step).random((R, V)) < keep
+    words = (V + 31) // 32
+    pad = np.zeros((R, words * 32), dtype=bool)
+    pad[:, :V] = allowed
+    w = pad.reshape(R, words, 32).astype(np.uint64) << np.arange(32, dtype=np.uint64)
+    return w.sum(axis=2).astype(np.uint32)
+
+
+def candidate_array(seed: int, B: int, M: int, V: int, kind: str = "normal") -> np.ndarray:
+    """fp32 [B*M, V] candidate scores with a chosen structure (top-k test inputs).
+
+    normal: -Gamma + N draws (distinct values); ties: values on a 0.25 grid;
+    equal: every value equal; sparse: -inf except ~1% finite; wide: values
+    spread over a range of ~4000; special: normal with NaN, +-0, +-inf mixed in.
+    """
+    rng = _rng(seed, "cand", 0, _KINDS.index(kind))
+    shape = (B * M, V)
+    if kind == "normal":
+        x = -rng.gamma(3.0, 3.0, size=(B * M, 1)) + rng.standard_normal(shape) * 3
+    elif kind == "ties":
+        x = np.round((-rng.gamma(3.0, 3.0, size=(B * M, 1)) + rng.standard_normal(shape) * 3) * 4) / 4
+    elif kind == "equal":
+        x = np.full(shape, -7.5)
+    elif kind == "sparse":
+        x = np.where(rng.random(shape) < 0.01, rng.standard_normal(shape), -np.inf)
+    elif kind == "wide":
+        x = rng.uniform(-4000.0, 0.0, size=shape)
+    elif kind == "special":
+        x = rng.standard_normal(shape) * 3
+        u = rng.random(shape)
+        x = np.where(u < 0.02, np.nan, x)
+        x = np.where((u >= 0.02) & (u < 0.05), 0.0, x)
+        x = np.where((u >= 0.05) & (u < 0.08), -0.0, x)
+        x = np.where((u >= 0.08) & (u < 0.10), -np.inf, x)
+        x = np.where((u >= 0.10) & (u < 0.101), np.inf, x)
+    else:
+        raise ValueError(kind)
+    return x.astype(np.float32)
+
+
+_KINDS = ["normal", "ties", "equal", "sparse", "wide", "special"]
+
+
+def dyn_parents(seed: int, step: int, B: int, M_prev: int, M_cur: int) -> np.ndarray:
+    """Request-local parents int32 [B*M_cur], uniform in [0, M_prev)."""
+    return _rng(seed, "dyn_parents", step).integers(0, M_prev, size=B * M_cur).astype(np.int32)

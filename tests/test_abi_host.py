@@ -29,7 +29,8 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ("grace_cross_attn", "grace_kv_append", "grace_self_attn_step",
-              "grace_self_attn_step_fused"):
+              "grace_self_attn_step_fused", "grace_self_attn_step_fused_dyn",
+              "grace_beam_scores", "grace_beam_topk", "grace_beam_topk_max_k"):
         assert n in names
 
 
@@ -148,6 +149,83 @@ def fused(**kw):
 ])
 def test_self_attn_fused_rejects(kw, status):
     assert fused(**kw) == status
+
+
+def fused_dyn(**kw):
+    # rows B*M_cur = 6 of 256 bytes; slab stride R_s rows
+    a = dict(q=ctypes.c_void_p(0x100000), kn=ctypes.c_void_p(0x200000), vn=ctypes.c_void_p(0x300000),
+             kp=ctypes.c_void_p(0x400000), vp=ctypes.c_void_p(0x500000), tp=ctypes.c_void_p(0x600000),
+             tn=ctypes.c_void_p(0x700000), par=ctypes.c_void_p(0x800000), B=2, Mp=2, Mc=3, Rs=8, H=2,
+             d=64, T=4, step=1, scale=0.125, dtype=1, out=ctypes.c_void_p(0x900000), err=None,
+             stream=None)
+    a.update(kw)
+    return G.library().grace_self_attn_step_fused_dyn(
+        a["q"], a["kn"], a["vn"], a["kp"], a["vp"], a["tp"], a["tn"], a["par"], a["B"], a["Mp"],
+        a["Mc"], a["Rs"], a["H"], a["d"], a["T"], a["step"], a["scale"], a["dtype"], a["out"],
+        a["err"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(Rs=5), G.GRACE_ERR_SHAPE),                       # R_s < B*M_cur
+    (dict(Mp=0), G.GRACE_ERR_SHAPE), (dict(Mp=5), G.GRACE_ERR_SHAPE),   # B*M_prev > R_s
+    (dict(Rs=1 << 29), G.GRACE_ERR_SHAPE),                 # T_max*R_s >= 2^31
+    (dict(step=4), G.GRACE_ERR_SHAPE), (dict(d=48), G.GRACE_ERR_UNSUPPORTED),
+    (dict(par=None), G.GRACE_ERR_NULL), (dict(q=None), G.GRACE_ERR_NULL),
+    (dict(out=ctypes.c_void_p(0x400000 + 8)), G.GRACE_ERR_ALIAS),          # out over slab 0
+    (dict(kn=ctypes.c_void_p(0x400000 + 8 * 256 + 16)), G.GRACE_ERR_ALIAS),  # inside slab 1
+    (dict(tn=ctypes.c_void_p(0x600000 + 4)), G.GRACE_ERR_ALIAS),
+    (dict(step=0, Mp=0, tp=None, par=None, B=0), G.GRACE_OK),
+])
+def test_self_attn_fused_dyn_rejects(kw, status):
+    assert fused_dyn(**kw) == status
+
+
+def beam_scores(**kw):
+    a = dict(lg=ctypes.c_void_p(0x100000), prev=ctypes.c_void_p(0x200000), mask=None, R=4, V=40,
+             dtype=1, cand=ctypes.c_void_p(0x300000), rmax=ctypes.c_void_p(0x400000), stream=None)
+    a.update(kw)
+    return G.library().grace_beam_scores(a["lg"], a["prev"], a["mask"], a["R"], a["V"], a["dtype"],
+                                         a["cand"], a["rmax"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(V=0), G.GRACE_ERR_SHAPE), (dict(R=-1), G.GRACE_ERR_SHAPE),
+    (dict(R=1 << 20, V=1 << 12), G.GRACE_ERR_SHAPE), (dict(dtype=2), G.GRACE_ERR_UNSUPPORTED),
+    (dict(lg=None), G.GRACE_ERR_NULL), (dict(cand=None), G.GRACE_ERR_NULL),
+    (dict(prev=None), G.GRACE_ERR_NULL),
+    (dict(cand=ctypes.c_void_p(0x100000 + 64)), G.GRACE_ERR_ALIAS),      # over logits
+    (dict(rmax=ctypes.c_void_p(0x300000 + 16)), G.GRACE_ERR_ALIAS),      # over cand
+    (dict(mask=ctypes.c_void_p(0x300000 + 4)), G.GRACE_ERR_ALIAS),       # cand over mask
+    (dict(R=0), G.GRACE_OK),
+])
+def test_beam_scores_rejects(kw, status):
+    assert beam_scores(**kw) == status
+
+
+def beam_topk(**kw):
+    a = dict(cand=ctypes.c_void_p(0x100000), rmax=None, B=2, M=8, V=64, k=16,
+             par=ctypes.c_void_p(0x200000), tok=ctypes.c_void_p(0x300000),
+             sc=ctypes.c_void_p(0x400000), stream=None)
+    a.update(kw)
+    return G.library().grace_beam_topk(a["cand"], a["rmax"], a["B"], a["M"], a["V"], a["k"], a["par"],
+                                       a["tok"], a["sc"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(k=0), G.GRACE_ERR_SHAPE), (dict(k=8 * 64 + 1), G.GRACE_ERR_SHAPE),
+    (dict(M=1 << 20, V=1 << 12, k=4), G.GRACE_ERR_SHAPE), (dict(M=0), G.GRACE_ERR_SHAPE),
+    (dict(M=100, k=5000), G.GRACE_ERR_SHAPE),              # above grace_beam_topk_max_k
+    (dict(cand=None), G.GRACE_ERR_NULL), (dict(tok=None), G.GRACE_ERR_NULL),
+    (dict(par=ctypes.c_void_p(0x300000 + 8)), G.GRACE_ERR_ALIAS),
+    (dict(sc=ctypes.c_void_p(0x100000 + 40)), G.GRACE_ERR_ALIAS),
+    (dict(B=0), G.GRACE_OK),
+])
+def test_beam_topk_rejects(kw, status):
+    assert beam_topk(**kw) == status
+
+
+def test_beam_topk_max_k():
+    assert G.library().grace_beam_topk_max_k() == 4096
 
 
 def test_binding_raises_without_library(monkeypatch, tmp_path):
