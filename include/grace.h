@@ -249,6 +249,9 @@ int32_t grace_beam_scores(const void* logits, const float* prev_scores, const ui
 /* Largest k grace_beam_topk accepts. */
 int32_t grace_beam_topk_max_k(void);
 
+/* Bytes of device workspace grace_beam_topk needs for B, M, V (-1 if out of range). */
+int64_t grace_beam_topk_workspace_bytes(int32_t B, int32_t M, int32_t V);
+
 /*
  * Per-request beam top-k (Sec. 3.1; with dynamic widths k = M_{t+1}, Sec. 3.3).
  * Request b owns candidates cand[b*M + m, v], flat index i = m*V + v.  The k
@@ -262,18 +265,22 @@ int32_t grace_beam_topk_max_k(void);
  * k beams are always produced; when fewer than k candidates are finite the
  * rest are filtered candidates (score -inf, dead beams).
  *
- *   cand      device, fp32 [B*M, V]
- *   row_max   device, fp32 [B*M] or NULL: a speed hint (grace_beam_scores'
- *             row maxima); any values give the same result
- *   B, M, V   requests, beams per request, vocabulary; M*V below 2^31
- *   k         1 <= k <= min(M*V, grace_beam_topk_max_k())
+ *   cand       device, fp32 [B*M, V]
+ *   row_max    device, fp32 [B*M] or NULL: a speed hint (grace_beam_scores'
+ *              row maxima); any values give the same result
+ *   B, M, V    requests, beams per request, vocabulary; M*V below 2^31
+ *   k          1 <= k <= min(M*V, grace_beam_topk_max_k())
+ *   workspace  device, at least grace_beam_topk_workspace_bytes(B, M, V) bytes,
+ *              8-byte aligned, caller-owned; contents on entry are ignored and
+ *              on return unspecified; calls that share it must not overlap
  *   parents, tokens   device, int32 [B, k];  scores  device, fp32 [B, k]
- *   stream    hipStream_t
- * Outputs must not overlap each other or the inputs.
+ *   stream     hipStream_t
+ * Outputs and the workspace must not overlap each other or the inputs; a
+ * workspace that is too small or misaligned is GRACE_ERR_SHAPE.
  */
 int32_t grace_beam_topk(const float* cand, const float* row_max, int32_t B, int32_t M, int32_t V,
-                        int32_t k, int32_t* parents, int32_t* tokens, float* scores,
-                        void* stream);
+                        int32_t k, void* workspace, int64_t workspace_bytes, int32_t* parents,
+                        int32_t* tokens, float* scores, void* stream);
 
 /* Human-readable name of a status code (static storage; never NULL). */
 const char* grace_status_string(int32_t status);

@@ -44,6 +44,7 @@ __device__ __forceinline__ float load_logit<uint16_t>(const uint16_t* p) {
 
 constexpr int kScoreThreads = 256;
 
+// Generic row kernel (any V): lanes stride over the row.
 template <class T>
 __global__ void __launch_bounds__(kScoreThreads)
 beam_scores_kernel(const T* __restrict__ logits, const float* __restrict__ prev,
@@ -69,6 +70,68 @@ beam_scores_kernel(const T* __restrict__ logits, const float* __restrict__ prev,
     const float s = ok ? p + (load_logit(x + v) - lse) : -INFINITY;
     out[v] = s;
     best = fmaxf(best, s);
+  }
+  best = wave_max(best);
+  if (row_max != nullptr && lane == 0) row_max[r] = best;
+}
+
+// Row kernel for V a multiple of 8, V <= 512*NCH: each lane owns runs of 8
+// consecutive tokens (one 16-byte bf16 load or two fp32 loads per run), the
+// row stays in registers across the max, sum and output passes.
+template <class T, int NCH>
+__global__ void __launch_bounds__(kScoreThreads)
+beam_scores_vec_kernel(const T* __restrict__ logits, const float* __restrict__ prev,
+                       const uint32_t* __restrict__ mask, float* __restrict__ cand,
+                       float* __restrict__ row_max, int32_t R, int32_t V) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * (kScoreThreads / 64) + (threadIdx.x >> 6);
+  if (r >= R) return;   // whole waves
+  const T* x = logits + r * V;
+  float f[NCH][8];
+  bool live[NCH];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int v0 = c * 512 + 8 * lane;
+    live[c] = v0 < V;
+    if (live[c]) {
+      if constexpr (sizeof(T) == 2) {
+        Chunk<BF16>::unpack(*(const u32x4*)(x + v0), f[c]);
+      } else {
+        Chunk<F32>::unpack(*(const u32x4*)(x + v0), f[c]);
+        Chunk<F32>::unpack(*(const u32x4*)(x + v0 + 4), f[c] + 4);
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) mx = fmaxf(mx, f[c][e]);
+    }
+  }
+  mx = wave_max(mx);
+  float z = 0.f;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c)
+    if (live[c]) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) z += expf(f[c][e] - mx);
+    }
+  z = wave_sum(z);
+  const float lse = mx + logf(z);
+  const float p = prev[r];
+  const int32_t words = (V + 31) >> 5;
+  float best = -INFINITY;
+  float* out = cand + r * V;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int v0 = c * 512 + 8 * lane;
+    if (!live[c]) continue;
+    const uint32_t bits = mask == nullptr ? 0xffu : (mask[r * words + (v0 >> 5)] >> (v0 & 31)) & 0xffu;
+    float o[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      o[e] = ((bits >> e) & 1u) ? p + (f[c][e] - lse) : -INFINITY;
+      best = fmaxf(best, o[e]);
+    }
+    *(u32x4*)(out + v0) = Chunk<F32>::pack(o);
+    *(u32x4*)(out + v0 + 4) = Chunk<F32>::pack(o + 4);
   }
   best = wave_max(best);
   if (row_max != nullptr && lane == 0) row_max[r] = best;
@@ -179,100 +242,244 @@ __device__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* scratch, uint32_t
   return before + v - x;
 }
 
+// ---- multi-workgroup fast path: slices of a request over several workgroups ----
+constexpr int kSliceThreads = 256;
+constexpr int kMaxSlices = 64;
+constexpr uint32_t kSliceTarget = 32768;   // candidates per slice (about)
+
+__host__ __device__ inline int topk_slices(uint32_t N) {
+  const uint32_t s = (N + kSliceTarget - 1) / kSliceTarget;
+  return (int)(s < 1 ? 1 : (s > (uint32_t)kMaxSlices ? (uint32_t)kMaxSlices : s));
+}
+
+// Workspace of one call (per request b): slice maxima [S], slice histograms
+// [S][kHistBins], info [4] = {b*, count above b*, gathered count, fast flag},
+// gathered list [kGatherCap] of composites.
+struct TopkWs {
+  float* smax;
+  uint32_t* hist;
+  int32_t* info;
+  uint64_t* list;
+  int S;
+  __host__ __device__ TopkWs(void* ws, int B, int S_) : S(S_) {
+    char* p = (char*)ws;
+    list = (uint64_t*)p;
+    p += (size_t)B * kGatherCap * 8;
+    hist = (uint32_t*)p;
+    p += (size_t)B * S_ * kHistBins * 4;
+    smax = (float*)p;
+    p += (size_t)B * S_ * 4;
+    info = (int32_t*)p;
+  }
+  __host__ __device__ static size_t bytes(int B, int S_) {
+    return (size_t)B * kGatherCap * 8 + (size_t)B * S_ * kHistBins * 4 + (size_t)B * S_ * 4 +
+           (size_t)B * 4 * 4;
+  }
+};
+
+__device__ __forceinline__ void slice_range(uint32_t N, int S, int s, uint32_t& i0, uint32_t& i1) {
+  const uint32_t per = (N + S - 1) / S;
+  i0 = min(N, (uint32_t)s * per);
+  i1 = min(N, i0 + per);
+}
+
+__device__ float block_max_256(float x, float* scratch) {
+  x = wave_max(x);
+  if ((threadIdx.x & 63) == 0) scratch[threadIdx.x >> 6] = x;
+  __syncthreads();
+  x = fmaxf(fmaxf(scratch[0], scratch[1]), fmaxf(scratch[2], scratch[3]));
+  __syncthreads();
+  return x;
+}
+
+__global__ void __launch_bounds__(kSliceThreads)
+topk_slice_max_kernel(const float* __restrict__ cand, const float* __restrict__ row_max,
+                      int32_t M, int32_t V, TopkWs ws) {
+  __shared__ float scratch[4];
+  const int s = blockIdx.x;
+  const int64_t b = blockIdx.y;
+  const uint32_t N = (uint32_t)M * (uint32_t)V;
+  uint32_t i0, i1;
+  slice_range(N, ws.S, s, i0, i1);
+  float best = -INFINITY;
+  if (row_max != nullptr) {
+    if (i1 > i0)
+      for (uint32_t m = i0 / V + threadIdx.x; m <= (i1 - 1) / V; m += kSliceThreads)
+        best = fmaxf(best, row_max[b * M + m]);
+  } else {
+    const float* c = cand + b * (int64_t)N;
+    for (uint32_t i = i0 + threadIdx.x; i < i1; i += kSliceThreads) best = fmaxf(best, c[i]);
+  }
+  best = block_max_256(best, scratch);
+  if (threadIdx.x == 0) ws.smax[b * ws.S + s] = best;
+}
+
+__device__ __forceinline__ float request_best(const TopkWs& ws, int64_t b) {
+  float best = -INFINITY;
+  for (int j = 0; j < ws.S; ++j) best = fmaxf(best, ws.smax[b * ws.S + j]);
+  return best;
+}
+
+__global__ void __launch_bounds__(kSliceThreads)
+topk_slice_hist_kernel(const float* __restrict__ cand, int32_t M, int32_t V, TopkWs ws) {
+  __shared__ uint32_t hist[kHistBins];
+  const int s = blockIdx.x;
+  const int64_t b = blockIdx.y;
+  const uint32_t N = (uint32_t)M * (uint32_t)V;
+  for (int i = threadIdx.x; i < kHistBins; i += kSliceThreads) hist[i] = 0u;
+  __syncthreads();
+  const float best = request_best(ws, b);
+  if (best == best && best > -INFINITY && best < INFINITY) {
+    const float lo = best - kWindow, inv_w = (float)kHistBins / kWindow;
+    uint32_t i0, i1;
+    slice_range(N, ws.S, s, i0, i1);
+    const float* c = cand + b * (int64_t)N;
+    // four candidates in flight per thread; one LDS atomic per counted candidate
+    for (uint32_t j0 = i0; j0 < i1; j0 += 4 * kSliceThreads) {
+      float x[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t i = j0 + u * kSliceThreads + threadIdx.x;
+        x[u] = i < i1 ? c[i] : -INFINITY;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int bin = window_bin(x[u], lo, inv_w);
+        if (bin > 0) atomicAdd(&hist[bin], 1u);
+      }
+    }
+  }
+  __syncthreads();
+  uint32_t* out = ws.hist + (b * ws.S + s) * (int64_t)kHistBins;
+  for (int i = threadIdx.x; i < kHistBins; i += kSliceThreads) out[i] = hist[i];
+}
+
+__global__ void __launch_bounds__(kTopkThreads)
+topk_boundary_kernel(int32_t k, TopkWs ws) {
+  __shared__ uint32_t scan[64];
+  const int tid = threadIdx.x;
+  const int64_t b = blockIdx.x;
+  __shared__ int32_t par[2];
+  if (tid < 2) par[tid] = 0;
+  // thread 0 owns the top 4 bins, in descending order
+  const int t_rev = kTopkThreads - 1 - tid;
+  uint32_t own[4] = {0u, 0u, 0u, 0u}, s4 = 0;
+  const uint32_t* h = ws.hist + b * ws.S * (int64_t)kHistBins;
+  for (int j = 0; j < ws.S; ++j)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) own[e] += h[(int64_t)j * kHistBins + 4 * t_rev + 3 - e];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) s4 += own[e];
+  __syncthreads();
+  uint32_t total;
+  const uint32_t before = block_exclusive_scan(s4, scan, &total);
+  if (before < (uint32_t)k && before + s4 >= (uint32_t)k) {
+    uint32_t run = before;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (run < (uint32_t)k && run + own[e] >= (uint32_t)k) {
+        par[0] = 4 * t_rev + 3 - e;
+        par[1] = (int32_t)run;
+        // fast only if everything in bins >= b* fits the gather list
+        par[0] = (par[0] > 0 && run + own[e] <= (uint32_t)kGatherCap) ? par[0] : 0;
+      }
+      run += own[e];
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const float best = request_best(ws, b);
+    const bool finite = best == best && best > -INFINITY && best < INFINITY;
+    const bool fast = finite && total >= (uint32_t)k && par[0] > 0;
+    ws.info[b * 4 + 0] = par[0];
+    ws.info[b * 4 + 1] = par[1];
+    ws.info[b * 4 + 2] = 0;          // gather counter
+    ws.info[b * 4 + 3] = fast ? 1 : 0;
+  }
+}
+
+// Gathered candidates are staged in LDS and flushed to the request's list
+// with one global atomic per flush (same-address global atomics serialise).
+constexpr int kStage = 2048;
+
+__global__ void __launch_bounds__(kSliceThreads)
+topk_gather_kernel(const float* __restrict__ cand, int32_t M, int32_t V, TopkWs ws) {
+  __shared__ uint64_t stage[kStage];
+  __shared__ uint32_t n_stage, base;
+  const int s = blockIdx.x;
+  const int64_t b = blockIdx.y;
+  if (ws.info[b * 4 + 3] == 0) return;   // whole workgroup
+  const int bstar = ws.info[b * 4 + 0];
+  const uint32_t N = (uint32_t)M * (uint32_t)V;
+  const float best = request_best(ws, b);
+  const float lo = best - kWindow, inv_w = (float)kHistBins / kWindow;
+  uint32_t i0, i1;
+  slice_range(N, ws.S, s, i0, i1);
+  const float* c = cand + b * (int64_t)N;
+  uint32_t* count = (uint32_t*)&ws.info[b * 4 + 2];
+  uint64_t* list = ws.list + b * (int64_t)kGatherCap;
+  if (threadIdx.x == 0) n_stage = 0;
+  __syncthreads();
+  auto flush = [&]() {
+    __syncthreads();
+    const uint32_t n = n_stage;
+    if (n > 0) {
+      if (threadIdx.x == 0) base = atomicAdd(count, n);
+      __syncthreads();
+      const uint32_t b0 = base;
+      for (uint32_t j = threadIdx.x; j < n; j += kSliceThreads)
+        if (b0 + j < (uint32_t)kGatherCap) list[b0 + j] = stage[j];
+      __syncthreads();
+      if (threadIdx.x == 0) n_stage = 0;
+    }
+    __syncthreads();
+  };
+  for (uint32_t j0 = i0; j0 < i1; j0 += 4 * kSliceThreads) {
+    float x[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint32_t i = j0 + u * kSliceThreads + threadIdx.x;
+      x[u] = i < i1 ? c[i] : -INFINITY;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint32_t i = j0 + u * kSliceThreads + threadIdx.x;
+      const int bin = window_bin(x[u], lo, inv_w);
+      wave_append(stage, &n_stage, i < i1 && bin >= bstar, composite(order_key(x[u]), i), kStage);
+    }
+    // at most 4 * kSliceThreads more per iteration: flush before the stage can overflow
+    __syncthreads();
+    if (n_stage > (uint32_t)(kStage - 4 * kSliceThreads)) flush();
+  }
+  flush();
+}
+
 struct TopkShared {
-  uint32_t hist[kHistBins];
+  uint32_t hist[256];
   uint64_t list[kGatherCap];
   uint32_t scan[64];
-  uint32_t count[4];
-  float fscratch[kTopkThreads / 64];
   int32_t ipar[4];
 };
 
+// Final selection: sort the gathered candidates (fast path), or an exact radix
+// select over all the request's candidates (fallback), then emit k in order.
 __global__ void __launch_bounds__(kTopkThreads)
-beam_topk_kernel(const float* __restrict__ cand, const float* __restrict__ row_max, int32_t M,
-                 int32_t V, int32_t k, int32_t* __restrict__ parents,
-                 int32_t* __restrict__ tokens, float* __restrict__ scores) {
+topk_final_kernel(const float* __restrict__ cand, int32_t M, int32_t V, int32_t k,
+                  TopkWs ws, int32_t* __restrict__ parents, int32_t* __restrict__ tokens,
+                  float* __restrict__ scores) {
   __shared__ TopkShared sh;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t b = blockIdx.x;
   const uint32_t N = (uint32_t)M * (uint32_t)V;
   const float* c = cand + b * (int64_t)N;
-
-  // ---- best score of the request ----
-  float best = -INFINITY;
-  if (row_max != nullptr) {
-    for (int32_t m = tid; m < M; m += kTopkThreads) best = fmaxf(best, row_max[b * M + m]);
-  } else {
-    for (uint32_t i = tid; i < N; i += kTopkThreads) best = fmaxf(best, c[i]);
-  }
-  best = wave_max(best);
-  if (lane == 0) sh.fscratch[wave] = best;
-  for (int i = tid; i < kHistBins; i += kTopkThreads) sh.hist[i] = 0u;
-  if (tid < 4) {
-    sh.count[tid] = 0u;
-    sh.ipar[tid] = 0;
-  }
-  __syncthreads();
-  best = -INFINITY;
-#pragma unroll
-  for (int w = 0; w < kTopkThreads / 64; ++w) best = fmaxf(best, sh.fscratch[w]);
-
-  bool fast = best == best && best > -INFINITY && best < INFINITY;
-  const float lo = best - kWindow;
-  const float inv_w = (float)kHistBins / kWindow;
-
-  // ---- fast path: window histogram (bin 0 is the catch-all, not counted) ----
-  uint32_t c_gt = 0, bstar = 0;
-  if (fast) {
-    for (uint32_t i0 = 0; i0 < N; i0 += kTopkThreads) {
-      const uint32_t i = i0 + tid;
-      const bool live = i < N;
-      const int bin = live ? window_bin(c[i], lo, inv_w) : 0;
-      hist_add(sh.hist, bin, live && bin > 0);
-    }
-    __syncthreads();
-    // suffix counts from the top bin: thread t owns bins [4t, 4t+4)
-    const int t_rev = kTopkThreads - 1 - tid;   // thread 0 owns the top 4 bins
-    uint32_t own[4], s4 = 0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      own[j] = sh.hist[4 * t_rev + 3 - j];   // descending bin order
-      s4 += own[j];
-    }
-    uint32_t total;
-    const uint32_t before = block_exclusive_scan(s4, sh.scan, &total);
-    // find the bin where the running count from the top reaches k
-    if (before < (uint32_t)k && before + s4 >= (uint32_t)k) {
-      uint32_t run = before;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if (run < (uint32_t)k && run + own[j] >= (uint32_t)k) {
-          sh.ipar[0] = 4 * t_rev + 3 - j;
-          sh.ipar[1] = (int32_t)run;
-        }
-        run += own[j];
-      }
-    }
-    if (tid == 0 && total < (uint32_t)k) sh.ipar[0] = 0;   // k-th lies in the catch-all
-    __syncthreads();
-    bstar = (uint32_t)sh.ipar[0];
-    c_gt = (uint32_t)sh.ipar[1];
-    fast = bstar > 0 && c_gt + sh.hist[bstar] <= (uint32_t)kGatherCap;
-  }
+  if (tid < 4) sh.ipar[tid] = 0;
 
   uint32_t n_sel;
-  if (fast) {
-    // ---- gather every candidate in bin >= b* and sort exactly ----
-    for (uint32_t i0 = 0; i0 < N; i0 += kTopkThreads) {
-      const uint32_t i = i0 + tid;
-      const bool live = i < N;
-      const float x = live ? c[i] : -INFINITY;
-      const int bin = live ? window_bin(x, lo, inv_w) : 0;
-      wave_append(sh.list, &sh.count[0], live && bin >= (int)bstar, composite(order_key(x), i),
-                  kGatherCap);
-    }
+  if (ws.info[b * 4 + 3] != 0) {
+    n_sel = (uint32_t)ws.info[b * 4 + 2];
+    const uint64_t* list = ws.list + b * (int64_t)kGatherCap;
+    for (uint32_t i = tid; i < n_sel; i += kTopkThreads) sh.list[i] = list[i];
     __syncthreads();
-    n_sel = sh.count[0];
   } else {
     // ---- exact radix select on the key, four 8-bit digits ----
     uint32_t prefix = 0, remaining = (uint32_t)k;
@@ -289,7 +496,7 @@ beam_topk_kernel(const float* __restrict__ cand, const float* __restrict__ row_m
       }
       __syncthreads();
       if (wave == 0) {
-        // digits from 255 down: 4 per lane, lane 0 owns 252..255
+        // digits from 255 down: 4 per lane, lane 0 owns 255..252
         uint32_t own[4], s4 = 0;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -330,8 +537,8 @@ beam_topk_kernel(const float* __restrict__ cand, const float* __restrict__ row_m
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const uint32_t i = i0 + 4 * tid + j;
-        keys[j] = i < N ? order_key(c[i]) : 0u;
         const bool in = i < N;
+        keys[j] = in ? order_key(c[i]) : 0u;
         ngt += in && keys[j] > T;
         neq += in && keys[j] == T;
       }
@@ -342,8 +549,9 @@ beam_topk_kernel(const float* __restrict__ cand, const float* __restrict__ row_m
       for (int j = 0; j < 4; ++j) {
         const uint32_t i = i0 + 4 * tid + j;
         if (i >= N) continue;
-        if (keys[j] > T) sh.list[pg++] = composite(keys[j], i);
-        else if (keys[j] == T) {
+        if (keys[j] > T) {
+          sh.list[pg++] = composite(keys[j], i);
+        } else if (keys[j] == T) {
           if (pe < need) sh.list[gt_total + pe] = composite(keys[j], i);
           ++pe;
         }
@@ -355,7 +563,7 @@ beam_topk_kernel(const float* __restrict__ cand, const float* __restrict__ row_m
     n_sel = (uint32_t)k;
   }
 
-  // ---- sort the gathered candidates, best first; emit the first k ----
+  // ---- sort the selected candidates, best first; emit the first k ----
   uint32_t n2 = 1;
   while (n2 < n_sel) n2 <<= 1;
   for (uint32_t i = n_sel + tid; i < n2; i += kTopkThreads) sh.list[i] = 0ull;
@@ -373,20 +581,53 @@ hipError_t launch_beam_scores(const void* logits, const float* prev, const uint3
                               float* cand, float* row_max, int32_t R, int32_t V, bool bf16,
                               hipStream_t stream) {
   const int64_t blocks = ((int64_t)R + kScoreThreads / 64 - 1) / (kScoreThreads / 64);
-  if (bf16)
-    hipLaunchKernelGGL(beam_scores_kernel<uint16_t>, dim3((unsigned)blocks), dim3(kScoreThreads),
-                       0, stream, (const uint16_t*)logits, prev, mask, cand, row_max, R, V);
-  else
-    hipLaunchKernelGGL(beam_scores_kernel<float>, dim3((unsigned)blocks), dim3(kScoreThreads), 0,
-                       stream, (const float*)logits, prev, mask, cand, row_max, R, V);
+  const dim3 grid((unsigned)blocks), block(kScoreThreads);
+#define GRACE_SC(TT, NCH)                                                                       \
+  hipLaunchKernelGGL((beam_scores_vec_kernel<TT, NCH>), grid, block, 0, stream,                 \
+                     (const TT*)logits, prev, mask, cand, row_max, R, V)
+  if (V % 8 == 0 && V <= 4096) {
+    const int nch = (V + 511) / 512;
+    if (bf16) {
+      if (nch == 1) GRACE_SC(uint16_t, 1);
+      else if (nch == 2) GRACE_SC(uint16_t, 2);
+      else if (nch <= 4) GRACE_SC(uint16_t, 4);
+      else GRACE_SC(uint16_t, 8);
+    } else {
+      if (nch == 1) GRACE_SC(float, 1);
+      else if (nch == 2) GRACE_SC(float, 2);
+      else if (nch <= 4) GRACE_SC(float, 4);
+      else GRACE_SC(float, 8);
+    }
+  } else if (bf16) {
+    hipLaunchKernelGGL(beam_scores_kernel<uint16_t>, grid, block, 0, stream,
+                       (const uint16_t*)logits, prev, mask, cand, row_max, R, V);
+  } else {
+    hipLaunchKernelGGL(beam_scores_kernel<float>, grid, block, 0, stream, (const float*)logits,
+                       prev, mask, cand, row_max, R, V);
+  }
+#undef GRACE_SC
   return hipGetLastError();
 }
 
+size_t beam_topk_workspace_bytes(int32_t B, int32_t M, int32_t V) {
+  return TopkWs::bytes(B, topk_slices((uint32_t)M * (uint32_t)V));
+}
+
 hipError_t launch_beam_topk(const float* cand, const float* row_max, int32_t B, int32_t M,
-                            int32_t V, int32_t k, int32_t* parents, int32_t* tokens,
-                            float* scores, hipStream_t stream) {
-  hipLaunchKernelGGL(beam_topk_kernel, dim3((unsigned)B), dim3(kTopkThreads), 0, stream, cand,
-                     row_max, M, V, k, parents, tokens, scores);
+                            int32_t V, int32_t k, void* workspace, int32_t* parents,
+                            int32_t* tokens, float* scores, hipStream_t stream) {
+  const int S = topk_slices((uint32_t)M * (uint32_t)V);
+  const TopkWs ws(workspace, B, S);
+  const dim3 slices((unsigned)S, (unsigned)B);
+  hipLaunchKernelGGL(topk_slice_max_kernel, slices, dim3(kSliceThreads), 0, stream, cand, row_max,
+                     M, V, ws);
+  hipLaunchKernelGGL(topk_slice_hist_kernel, slices, dim3(kSliceThreads), 0, stream, cand, M, V,
+                     ws);
+  hipLaunchKernelGGL(topk_boundary_kernel, dim3((unsigned)B), dim3(kTopkThreads), 0, stream, k,
+                     ws);
+  hipLaunchKernelGGL(topk_gather_kernel, slices, dim3(kSliceThreads), 0, stream, cand, M, V, ws);
+  hipLaunchKernelGGL(topk_final_kernel, dim3((unsigned)B), dim3(kTopkThreads), 0, stream, cand, M,
+                     V, k, ws, parents, tokens, scores);
   return hipGetLastError();
 }
 

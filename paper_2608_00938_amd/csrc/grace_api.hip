@@ -241,24 +241,31 @@ int32_t grace_beam_scores(const void* logits, const float* prev_scores, const ui
 
 int32_t grace_beam_topk_max_k(void) { return grace::beam_topk_max_k(); }
 
+int64_t grace_beam_topk_workspace_bytes(int32_t B, int32_t M, int32_t V) {
+  if (B < 0 || M < 1 || V < 1 || (int64_t)M * V >= ((int64_t)1 << 31)) return -1;
+  return (int64_t)grace::beam_topk_workspace_bytes(B, M, V);
+}
+
 int32_t grace_beam_topk(const float* cand, const float* row_max, int32_t B, int32_t M, int32_t V,
-                        int32_t k, int32_t* parents, int32_t* tokens, float* scores,
-                        void* stream) {
+                        int32_t k, void* workspace, int64_t workspace_bytes, int32_t* parents,
+                        int32_t* tokens, float* scores, void* stream) {
   if (B < 0 || M < 1 || V < 1 || (int64_t)M * V >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
   if (k < 1 || k > grace::beam_topk_max_k() || (int64_t)k > (int64_t)M * V) return GRACE_ERR_SHAPE;
   if ((int64_t)B * k >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
   if (B == 0) return GRACE_OK;
-  if (!cand || !parents || !tokens || !scores) return GRACE_ERR_NULL;
+  if (!cand || !parents || !tokens || !scores || !workspace) return GRACE_ERR_NULL;
+  const int64_t ws_need = (int64_t)grace::beam_topk_workspace_bytes(B, M, V);
+  if (workspace_bytes < ws_need || ((uintptr_t)workspace & 7) != 0) return GRACE_ERR_SHAPE;
   const int64_t n = (int64_t)B * M * V * 4, outb = (int64_t)B * k * 4;
-  const Range outs[3] = {{parents, outb}, {tokens, outb}, {scores, outb}};
-  for (int i = 0; i < 3; ++i) {
-    for (int j = i + 1; j < 3; ++j)
+  const Range outs[4] = {{parents, outb}, {tokens, outb}, {scores, outb}, {workspace, ws_need}};
+  for (int i = 0; i < 4; ++i) {
+    for (int j = i + 1; j < 4; ++j)
       if (overlaps(outs[i].p, outs[i].n, outs[j].p, outs[j].n)) return GRACE_ERR_ALIAS;
     if (overlaps(outs[i].p, outs[i].n, cand, n)) return GRACE_ERR_ALIAS;
     if (row_max && overlaps(outs[i].p, outs[i].n, row_max, (int64_t)B * M * 4)) return GRACE_ERR_ALIAS;
   }
-  return hip_status(grace::launch_beam_topk(cand, row_max, B, M, V, k, parents, tokens, scores,
-                                            (hipStream_t)stream));
+  return hip_status(grace::launch_beam_topk(cand, row_max, B, M, V, k, workspace, parents, tokens,
+                                            scores, (hipStream_t)stream));
 }
 
 }  // extern "C"

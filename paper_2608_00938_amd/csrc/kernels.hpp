@@ -40,10 +40,12 @@ hipError_t launch_beam_scores(const void* logits, const float* prev, const uint3
                               float* cand, float* row_max, int32_t R, int32_t V, bool bf16,
                               hipStream_t stream);
 
-// Per-request top-k over M*V candidates; k <= beam_topk_max_k().
+// Per-request top-k over M*V candidates; k <= beam_topk_max_k(); workspace of
+// beam_topk_workspace_bytes(B, M, V) bytes, 8-byte aligned.
 hipError_t launch_beam_topk(const float* cand, const float* row_max, int32_t B, int32_t M,
-                            int32_t V, int32_t k, int32_t* parents, int32_t* tokens,
-                            float* scores, hipStream_t stream);
+                            int32_t V, int32_t k, void* workspace, int32_t* parents,
+                            int32_t* tokens, float* scores, hipStream_t stream);
+size_t beam_topk_workspace_bytes(int32_t B, int32_t M, int32_t V);
 int32_t beam_topk_max_k();
 
 }  // namespace grace

@@ -42,8 +42,9 @@ _SIGNATURES = {
     "grace_beam_scores": [_c_void_p, _c_void_p, _c_void_p, _c_int, _c_int, _c_int, _c_void_p,
                           _c_void_p, _c_void_p],
     "grace_beam_topk_max_k": [],
+    "grace_beam_topk_workspace_bytes": [_c_int, _c_int, _c_int],
     "grace_beam_topk": [_c_void_p, _c_void_p, _c_int, _c_int, _c_int, _c_int, _c_void_p,
-                        _c_void_p, _c_void_p, _c_void_p],
+                        ctypes.c_int64, _c_void_p, _c_void_p, _c_void_p, _c_void_p],
     "grace_status_string": [_c_int],
     "grace_last_hip_error": [],
     "grace_abi_version": [],
@@ -70,7 +71,8 @@ def library() -> ctypes.CDLL:
         for name, args in _SIGNATURES.items():
             fn = getattr(lib, name)
             fn.argtypes = args
-            fn.restype = ctypes.c_char_p if name == "grace_status_string" else _c_int
+            fn.restype = (ctypes.c_char_p if name == "grace_status_string" else
+                          ctypes.c_int64 if name.endswith("_bytes") else _c_int)
         _lib = lib
     return _lib
 
@@ -204,20 +206,30 @@ def grace_beam_topk_max_k() -> int:
     return library().grace_beam_topk_max_k()
 
 
+def grace_beam_topk_workspace_bytes(B: int, M: int, V: int) -> int:
+    return library().grace_beam_topk_workspace_bytes(B, M, V)
+
+
 def grace_beam_topk(cand, B: int, M: int, k: int, row_max=None, parents=None, tokens=None,
-                    scores=None):
+                    scores=None, workspace=None):
     """Per-request top-k over cand [B*M, V] fp32.  Returns (parents, tokens, scores),
-    each [B, k] (int32, int32, fp32), best first."""
-    _contig(cand, row_max, parents, tokens, scores)
+    each [B, k] (int32, int32, fp32), best first.  ``workspace``: a device uint8
+    tensor of at least grace_beam_topk_workspace_bytes(B, M, V) bytes (allocated
+    here when not given)."""
+    _contig(cand, row_max, parents, tokens, scores, workspace)
     V = cand.shape[1]
     dev = cand.device
+    need = grace_beam_topk_workspace_bytes(B, M, V)
+    if workspace is None:
+        workspace = torch.empty((max(need, 8),), dtype=torch.uint8, device=dev)
     if parents is None:
         parents = torch.empty((B, k), dtype=torch.int32, device=dev)
     if tokens is None:
         tokens = torch.empty((B, k), dtype=torch.int32, device=dev)
     if scores is None:
         scores = torch.empty((B, k), dtype=torch.float32, device=dev)
-    st = library().grace_beam_topk(_ptr(cand), _ptr(row_max), B, M, V, k, _ptr(parents),
+    st = library().grace_beam_topk(_ptr(cand), _ptr(row_max), B, M, V, k, _ptr(workspace),
+                                   workspace.numel() * workspace.element_size(), _ptr(parents),
                                    _ptr(tokens), _ptr(scores), _stream(cand))
     _check(st, "grace_beam_topk")
     return parents, tokens, scores

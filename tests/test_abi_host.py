@@ -30,7 +30,8 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ("grace_cross_attn", "grace_kv_append", "grace_self_attn_step",
               "grace_self_attn_step_fused", "grace_self_attn_step_fused_dyn",
-              "grace_beam_scores", "grace_beam_topk", "grace_beam_topk_max_k"):
+              "grace_beam_scores", "grace_beam_topk", "grace_beam_topk_max_k",
+              "grace_beam_topk_workspace_bytes"):
         assert n in names
 
 
@@ -204,11 +205,12 @@ def test_beam_scores_rejects(kw, status):
 
 def beam_topk(**kw):
     a = dict(cand=ctypes.c_void_p(0x100000), rmax=None, B=2, M=8, V=64, k=16,
+             ws=ctypes.c_void_p(0x1000000), wsb=1 << 22,
              par=ctypes.c_void_p(0x200000), tok=ctypes.c_void_p(0x300000),
              sc=ctypes.c_void_p(0x400000), stream=None)
     a.update(kw)
-    return G.library().grace_beam_topk(a["cand"], a["rmax"], a["B"], a["M"], a["V"], a["k"], a["par"],
-                                       a["tok"], a["sc"], a["stream"])
+    return G.library().grace_beam_topk(a["cand"], a["rmax"], a["B"], a["M"], a["V"], a["k"], a["ws"],
+                                       a["wsb"], a["par"], a["tok"], a["sc"], a["stream"])
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -218,14 +220,22 @@ def beam_topk(**kw):
     (dict(cand=None), G.GRACE_ERR_NULL), (dict(tok=None), G.GRACE_ERR_NULL),
     (dict(par=ctypes.c_void_p(0x300000 + 8)), G.GRACE_ERR_ALIAS),
     (dict(sc=ctypes.c_void_p(0x100000 + 40)), G.GRACE_ERR_ALIAS),
+    (dict(ws=None), G.GRACE_ERR_NULL), (dict(wsb=1024), G.GRACE_ERR_SHAPE),
+    (dict(ws=ctypes.c_void_p(0x1000004)), G.GRACE_ERR_SHAPE),          # misaligned
+    (dict(ws=ctypes.c_void_p(0x100000 + 64)), G.GRACE_ERR_ALIAS),      # over cand
     (dict(B=0), G.GRACE_OK),
 ])
 def test_beam_topk_rejects(kw, status):
     assert beam_topk(**kw) == status
 
 
-def test_beam_topk_max_k():
+def test_beam_topk_max_k_and_workspace():
     assert G.library().grace_beam_topk_max_k() == 4096
+    lib = G.library()
+    assert lib.grace_beam_topk_workspace_bytes(0, 1, 1) >= 0
+    assert lib.grace_beam_topk_workspace_bytes(2, 0, 64) == -1
+    small, big = lib.grace_beam_topk_workspace_bytes(1, 8, 64), lib.grace_beam_topk_workspace_bytes(64, 4096, 512)
+    assert 0 < small < big < (128 << 20)
 
 
 def test_binding_raises_without_library(monkeypatch, tmp_path):
