@@ -19,7 +19,9 @@
  *                         filtered tokens removed (Sec. 3.1);
  *   grace_beam_topk       per-request top-k that yields the next step's beams,
  *                         i.e. the parents the rearrangement consumes (Sec. 3.1,
- *                         Sec. 3.3).
+ *                         Sec. 3.3);
+ *   grace_graph_*         capture of a sequence of these calls (a whole decode
+ *                         loop) as one replayable HIP graph (Sec. 5).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -281,6 +283,32 @@ int64_t grace_beam_topk_workspace_bytes(int32_t B, int32_t M, int32_t V);
 int32_t grace_beam_topk(const float* cand, const float* row_max, int32_t B, int32_t M, int32_t V,
                         int32_t k, void* workspace, int64_t workspace_bytes, int32_t* parents,
                         int32_t* tokens, float* scores, void* stream);
+
+/*
+ * Graph capture (Sec. 5: the fixed-length decoding loop is captured as one
+ * graph).  Every entry point above only enqueues kernels on its stream; it
+ * never allocates, synchronises or sets memory, so calls made on `stream`
+ * between grace_graph_begin and grace_graph_end are recorded, not run, and the
+ * returned executable graph replays them all with one grace_graph_launch.
+ * Pointers and sizes are frozen at capture: a replay reads and writes the same
+ * buffers, which the caller keeps alive until grace_graph_destroy.
+ *
+ *   grace_graph_begin(stream)            start capturing on `stream` (hipStream_t,
+ *                                        not NULL: the null stream cannot be
+ *                                        captured); thread-local capture mode
+ *   grace_graph_end(stream, &exec)       stop capturing, instantiate; *exec receives
+ *                                        the executable graph (NULL on failure)
+ *   grace_graph_launch(exec, stream)     replay on `stream`
+ *   grace_graph_destroy(exec)            free the executable graph (NULL is a no-op)
+ *   grace_graph_last_hip_error()         hipError_t of the last failed graph call
+ *                                        in this thread
+ * Each returns GRACE_OK, GRACE_ERR_NULL or GRACE_ERR_HIP.
+ */
+int32_t grace_graph_begin(void* stream);
+int32_t grace_graph_end(void* stream, void** graph_exec);
+int32_t grace_graph_launch(void* graph_exec, void* stream);
+int32_t grace_graph_destroy(void* graph_exec);
+int32_t grace_graph_last_hip_error(void);
 
 /* Human-readable name of a status code (static storage; never NULL). */
 const char* grace_status_string(int32_t status);

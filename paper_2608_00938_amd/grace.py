@@ -45,6 +45,11 @@ _SIGNATURES = {
     "grace_beam_topk_workspace_bytes": [_c_int, _c_int, _c_int],
     "grace_beam_topk": [_c_void_p, _c_void_p, _c_int, _c_int, _c_int, _c_int, _c_void_p,
                         ctypes.c_int64, _c_void_p, _c_void_p, _c_void_p, _c_void_p],
+    "grace_graph_begin": [_c_void_p],
+    "grace_graph_end": [_c_void_p, ctypes.POINTER(_c_void_p)],
+    "grace_graph_launch": [_c_void_p, _c_void_p],
+    "grace_graph_destroy": [_c_void_p],
+    "grace_graph_last_hip_error": [],
     "grace_status_string": [_c_int],
     "grace_last_hip_error": [],
     "grace_abi_version": [],
@@ -233,6 +238,43 @@ def grace_beam_topk(cand, B: int, M: int, k: int, row_max=None, parents=None, to
                                    _ptr(tokens), _ptr(scores), _stream(cand))
     _check(st, "grace_beam_topk")
     return parents, tokens, scores
+
+
+class Graph:
+    """An executable HIP graph recorded from library calls (grace_graph_*)."""
+
+    def __init__(self, handle: int):
+        self.handle = handle
+
+    def launch(self, stream=None):
+        st = torch.cuda.current_stream() if stream is None else stream
+        _check(library().grace_graph_launch(self.handle, st.cuda_stream), "grace_graph_launch")
+
+    def destroy(self):
+        if self.handle:
+            library().grace_graph_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+
+def capture(fn, stream) -> Graph:
+    """Record the library calls ``fn()`` enqueues on ``stream`` (a torch.cuda.Stream
+    other than the null stream) into a Graph; nothing runs until Graph.launch."""
+    lib = library()
+    with torch.cuda.stream(stream):
+        _check(lib.grace_graph_begin(stream.cuda_stream), "grace_graph_begin")
+        try:
+            fn()
+        finally:
+            h = _c_void_p()
+            st = lib.grace_graph_end(stream.cuda_stream, ctypes.byref(h))
+    _check(st, "grace_graph_end")
+    return Graph(h.value)
 
 
 class KVCache:

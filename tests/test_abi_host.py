@@ -238,6 +238,16 @@ def test_beam_topk_max_k_and_workspace():
     assert 0 < small < big < (128 << 20)
 
 
+def test_graph_api_rejects_null():
+    lib = G.library()
+    h = ctypes.c_void_p()
+    assert lib.grace_graph_begin(None) == G.GRACE_ERR_NULL
+    assert lib.grace_graph_end(None, ctypes.byref(h)) == G.GRACE_ERR_NULL
+    assert lib.grace_graph_end(P, None) == G.GRACE_ERR_NULL
+    assert lib.grace_graph_launch(None, None) == G.GRACE_ERR_NULL
+    assert lib.grace_graph_destroy(None) == G.GRACE_OK
+
+
 def test_binding_raises_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(G, "_lib", None)
     monkeypatch.setattr(G, "_LIB_PATH", str(tmp_path / "missing.so"))

@@ -1,0 +1,125 @@
+"""A whole decode loop (layers x steps of cross-attention and fused paged
+self-attention, then score update and top-k feeding the next step's parents)
+recorded as one HIP graph replays bit-identically to the same loop run eagerly.
+
+The graph is replayed several times with eager library work, host
+synchronisations and overwritten outputs in between; every replay must
+reproduce every output of the eager run exactly.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_00938_amd import decode as D
+from paper_2608_00938_amd import grace as G
+from paper_2608_00938_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _make_loop(dev, B=2, widths=(1, 8, 16, 16), H=2, d=64, V=64, layers=2, L=24, seed=31):
+    wl = W.custom(dtype="bf16", B=B, M=max(widths), H=H, d=d, steps=len(widths), L=L)
+    inp = W.DecodeInputs(wl, seed, dev)
+    ek, ev = inp.enc_kv
+    off = inp.offsets_tensor()
+    step_inputs = []
+    for l in range(layers):
+        per = []
+        for t, M in enumerate(widths):
+            g = lambda tag: W.normal((B * M, H, d), seed + 100 * l, tag, t, wl, dev)  # noqa: E731
+            per.append(dict(q_cross=g("q_cross"), q_self=g("q_self"), k_new=g("k_new"),
+                            v_new=g("v_new")))
+        step_inputs.append(per)
+    logits = [W.beam_logits(seed, t, B * M, V, "bf16", dev) for t, M in enumerate(widths)]
+    masks = [torch.from_numpy(W.beam_mask(seed, t, B * M, V, keep=0.7).view(np.int32)).to(dev)
+             for t, M in enumerate(widths)]
+    loop = D.DecodeLoop(B, widths, H, d, V, layers, ek, ev, off, step_inputs, logits, masks)
+    return loop, inp
+
+
+def _snapshot(loop):
+    outs = []
+    for l in range(loop.layers):
+        outs += [x.clone() for x in loop.x_cross[l]] + [x.clone() for x in loop.x_self[l]]
+    outs += [x.clone() for x in loop.parents + loop.tokens + loop.scores]
+    return outs + [x.clone() for x in _written_slabs(loop)]
+
+
+def _written_slabs(loop):
+    """The pool rows the loop writes: slab t, rows 0 .. B*M_t - 1 (the rest is padding)."""
+    out = []
+    for c in loop.caches:
+        for t, M in enumerate(loop.widths):
+            out += [c.k_pool[t, :loop.B * M], c.v_pool[t, :loop.B * M]]
+    return out
+
+
+def _current(loop):
+    outs = []
+    for l in range(loop.layers):
+        outs += list(loop.x_cross[l]) + list(loop.x_self[l])
+    outs += list(loop.parents + loop.tokens + loop.scores)
+    return outs + _written_slabs(loop)
+
+
+def test_decode_loop_graph_replays_match_eager(gpu):
+    loop, _ = _make_loop(gpu)
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        loop.run()
+    stream.synchronize()
+    ref = _snapshot(loop)
+    _log(f"[graph] eager loop done; {len(ref)} outputs")
+    graph = loop.capture(stream)
+    other, _ = _make_loop(gpu, seed=77)          # unrelated eager work between replays
+    for rep in range(3):
+        for x in _current(loop):
+            x.fill_(-1) if x.dtype in (torch.int32,) else x.fill_(float("nan"))
+        with torch.cuda.stream(stream):
+            other.run()
+        torch.cuda.synchronize()
+        graph.launch(stream)
+        stream.synchronize()
+        for i, (a, b) in enumerate(zip(_current(loop), ref)):
+            same = torch.equal(a.view(torch.uint8) if a.dtype != torch.int32 else a,
+                               b.view(torch.uint8) if b.dtype != torch.int32 else b)
+            assert same, f"replay {rep}: output {i} differs"
+        _log(f"  replay {rep}: all outputs identical to the eager run")
+    graph.destroy()
+
+
+def test_decode_loop_wiring(gpu):
+    """Step 0 cross-attention matches the oracle; every row's table starts with
+    its request's step-0 block (M_0 = 1 beam per request: every beam descends
+    from it), checked on the last step's table."""
+    loop, inp = _make_loop(gpu)
+    loop.run()
+    torch.cuda.synchronize()
+    f = lambda t: t.float().cpu().numpy().astype(np.float64)  # noqa: E731
+    q = loop.inputs[0][0]["q_cross"]
+    ref = oracle.cross_attn(f(q), f(loop.enc_k), f(loop.enc_v), inp.offsets, loop.widths[0],
+                            1 / math.sqrt(loop.d))
+    assert np.max(np.abs(f(loop.x_cross[0][0]) - ref)) <= 2e-2
+    assert int(loop.parents[0].max()) == 0 and int(loop.parents[0].min()) == 0
+    t = loop.T - 1
+    Mt = loop.widths[t]
+    for c in loop.caches:
+        tab = c.table(t)[:loop.B * Mt].cpu().numpy()
+        assert tab[:, 0].tolist() == [r // Mt for r in range(loop.B * Mt)]
+        assert tab[:, t].tolist() == [t * c.B * c.M + r for r in range(loop.B * Mt)]
+    for c in loop.caches:
+        assert int(c.err_flag.item()) == 0
+
+
+def test_graph_capture_on_null_stream_is_refused(gpu):
+    with pytest.raises(G.GraceError):
+        G.capture(lambda: None, torch.cuda.default_stream())
