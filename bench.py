@@ -127,6 +127,86 @@ def cpu_baseline(wl, inp, parents, budget_s=12.0):
                       f"{elapsed:.1f} s measured, scaled x{wl.B / nreq:.1f}"}
 
 
+def bench_beam_step(wl, dev, reps=10):
+    """Side measurement (not part of `value`): score update + top-k of one step at
+    the workload's shape, vocabulary 512, k = M, synthetic bf16 logits and a
+    60 % filter; HIP events on the current stream, medians."""
+    import torch
+    from paper_2608_00938_amd import grace as G
+    from paper_2608_00938_amd import workloads as W
+    B, M, V, k = wl.B, wl.M, W.VOCAB, wl.M
+    R = B * M
+    logits = W.beam_logits(0, 2, R, V, "bf16", dev)
+    prev = torch.from_numpy(W.beam_prev_scores(0, 2, R)).to(dev)
+    mask = torch.from_numpy(W.beam_mask(0, 2, R, V).view(np.int32)).to(dev)
+    cand = torch.empty((R, V), dtype=torch.float32, device=dev)
+    rmax = torch.empty((R,), dtype=torch.float32, device=dev)
+    par = torch.empty((B, k), dtype=torch.int32, device=dev)
+    tok = torch.empty_like(par)
+    sc = torch.empty((B, k), dtype=torch.float32, device=dev)
+    ws = torch.empty((G.grace_beam_topk_workspace_bytes(B, M, V),), dtype=torch.uint8, device=dev)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    ts, tk = [], []
+    for i in range(reps + 2):
+        ev[0].record()
+        G.grace_beam_scores(logits, prev, mask, cand=cand, row_max=rmax)
+        ev[1].record()
+        G.grace_beam_topk(cand, B, M, k, row_max=rmax, parents=par, tokens=tok, scores=sc,
+                          workspace=ws)
+        ev[2].record()
+        torch.cuda.synchronize()
+        if i >= 2:
+            ts.append(ev[0].elapsed_time(ev[1]))
+            tk.append(ev[1].elapsed_time(ev[2]))
+    us_s, us_k = float(np.median(ts)) * 1e3, float(np.median(tk)) * 1e3
+    words = (V + 31) // 32
+    bytes_s = R * V * 2 + R * 4 + R * words * 4 + R * V * 4 + R * 4
+    return {"shape": f"{B} req x {M} beams x {V} tokens, k={k}", "scores_us": round(us_s, 1),
+            "scores_GBs": round(bytes_s / (us_s * 1e-6) / 1e9, 1), "topk_us": round(us_k, 1),
+            "note": "side measurement, not part of value"}
+
+
+def bench_decode_loop(dev, name="bf16_b8_m256", layers=3, reps=20):
+    """Side measurement: a whole decode loop (layers x steps of cross-attention and
+    fused paged self-attention, score update and top-k feeding the next step)
+    launched call by call vs replayed as one captured graph."""
+    import torch
+    from paper_2608_00938_amd import decode as D
+    from paper_2608_00938_amd import workloads as W
+    wl = W.WORKLOADS[name]
+    inp = W.DecodeInputs(wl, 0, dev)
+    ek, ev_ = inp.enc_kv
+    shp = (wl.R, wl.H, wl.d)
+    si = [[{tag: W.normal(shp, l, tag, t, wl, dev) for tag in ("q_cross", "q_self", "k_new", "v_new")}
+           for t in range(wl.steps)] for l in range(layers)]
+    logits = [W.beam_logits(0, t, wl.R, W.VOCAB, "bf16", dev) for t in range(wl.steps)]
+    loop = D.DecodeLoop(wl.B, [wl.M] * wl.steps, wl.H, wl.d, W.VOCAB, layers, ek, ev_,
+                        inp.offsets_tensor(), si, logits)
+    s = torch.cuda.Stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(s):
+        for _ in range(3):
+            loop.run()
+        e0.record(s)
+        for _ in range(reps):
+            loop.run()
+        e1.record(s)
+    s.synchronize()
+    eager = e0.elapsed_time(e1) / reps * 1e3
+    g = loop.capture(s)
+    for _ in range(3):
+        g.launch(s)
+    e0.record(s)
+    for _ in range(reps):
+        g.launch(s)
+    e1.record(s)
+    s.synchronize()
+    graph = e0.elapsed_time(e1) / reps * 1e3
+    g.destroy()
+    return {"workload": name, "layers": layers, "steps": wl.steps, "eager_us": round(eager, 1),
+            "graph_us": round(graph, 1), "note": "side measurement, not part of value"}
+
+
 def torch_index(a):
     import torch
     return torch.from_numpy(np.ascontiguousarray(a))
@@ -141,6 +221,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--path", choices=("fused", "split"), default="fused",
                     help="self-attention as one fused append+attend call, or append then attend")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the side measurements (beam step, graph-captured decode loop)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one device copy of this many MiB first (reference for HBM counters)")
     ap.add_argument("--workload", default=WORKLOAD, help=argparse.SUPPRESS)
@@ -304,6 +386,11 @@ def main():
         "hbm": hbm,
         "event_step_ms_median": round(float(np.median(step_ms)), 4),
     }
+    if not args.no_extras:
+        del steps, cache
+        torch.cuda.empty_cache()
+        result["beam_step"] = bench_beam_step(wl, dev)
+        result["decode_loop_graph"] = bench_decode_loop(dev)
     if not args.no_cpu_baseline:
         log("timing the oracle on host cores ...")
         result["cpu_baseline"] = cpu_baseline(wl, inp, parents_np)
