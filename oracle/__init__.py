@@ -6,3 +6,4 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 from .grace_oracle import *  # noqa: F401,F403
 from .grace_oracle import __all__  # noqa: F401
 from . import beam_oracle  # noqa: F401,E402
+from . import gtm_oracle  # noqa: F401,E402

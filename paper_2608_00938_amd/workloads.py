@@ -36,7 +36,7 @@ _TORCH_DTYPE = {F32: torch.float32, BF16: torch.bfloat16}
 # Tensor tags used in the per-tensor seed.
 _TAG = {"enc_k": 1, "enc_v": 2, "q_cross": 3, "q_self": 4, "k_new": 5, "v_new": 6,
         "parents": 7, "lengths": 8, "perm": 9, "logits": 10, "prev_scores": 11, "mask": 12,
-        "cand": 13, "dyn_parents": 14}
+        "cand": 13, "dyn_parents": 14, "sids": 15, "ads": 16, "users": 17, "beam_nodes": 18}
 
 # Beam step shapes of the paper's model (Sec. 3.2, Sec. 3.3): SID-token
 # vocabulary and the dynamic per-step beam widths (M_1, ..., M_4).
@@ -259,3 +259,147 @@ _KINDS = ["normal", "ties", "equal", "sparse", "wide", "special"]
 def dyn_parents(seed: int, step: int, B: int, M_prev: int, M_cur: int) -> np.ndarray:
     """Request-local parents int32 [B*M_cur], uniform in [0, M_prev)."""
     return _rng(seed, "dyn_parents", step).integers(0, M_prev, size=B * M_cur).astype(np.int32)
+
+
+# ---------------------------------------------------------------------------
+# Synthetic CD+GTM index (Sec. 6, App. A) and request attributes.  The paper's
+# 30M-SID index and its targeting data are not public; this builds an index of
+# the same form: a SID trie in CSR form whose child entries point to
+# deduplicated bitmask (W_bm = 7 words) and Bloom (W_bl = 4 words) matcher rows,
+# each node matcher the OR of the matchers of the ads below it.
+#   SIDs: length 4 over |V| = 512; level l draws a Zipf(1.0) rank over C_l
+#         choices (512, 128, 64, 32), mapped to a token by a per-prefix
+#         bijection, so prefixes cluster as semantic IDs do.
+#   Ads per SID: 1 + Geometric(0.7), capped at 11 (p50 1, p90 2 as in the
+#         paper's index summary).
+#   Bitmask: attributes of 200, 8, 4, 64 and 32 values (country, age, gender,
+#         language, device) packed into 7 words; an ad allows every value of an
+#         attribute with probability 0.5, else 1-5 random values.
+#   Bloom: 256 bits, 3 hash bits per location id out of 10000; an ad targets
+#         any location (all ones) with probability 0.4, else 1-8 locations.
+#   Users: one value per attribute; 1-64 locations (most requests 1-8).
+# ---------------------------------------------------------------------------
+GTM_ATTRS = (200, 8, 4, 64, 32)
+GTM_W_BM, GTM_W_BL, GTM_BLOOM_BITS, GTM_LOCS = 7, 4, 256, 10000
+
+
+def _bloom_bits(loc: np.ndarray) -> np.ndarray:
+    """Three bit positions in [0, 256) per location id (multiplicative hashing)."""
+    loc = loc.astype(np.uint64)
+    mults = np.array([0x9E3779B97F4A7C15, 0xC2B2AE3D27D4EB4F, 0x165667B19E3779F9], dtype=np.uint64)
+    h = (loc[..., None] * mults) >> np.uint64(56)
+    return h.astype(np.int64)
+
+
+def _set_bits(words: np.ndarray, rows: np.ndarray, bits: np.ndarray):
+    np.bitwise_or.at(words, (rows, bits // 64), np.left_shift(np.uint64(1), (bits % 64).astype(np.uint64)))
+
+
+def gtm_index(seed: int, n_sids: int, V: int = 512, sid_len: int = 4) -> dict:
+    rng = _rng(seed, "sids")
+    choices = [V, 128, 64, 32][:sid_len]
+    sids = np.empty((n_sids, sid_len), dtype=np.int64)
+    key = np.zeros(n_sids, dtype=np.uint64)
+    for l, C in enumerate(choices):
+        w = 1.0 / np.arange(1, C + 1)
+        rank = rng.choice(C, size=n_sids, p=w / w.sum()).astype(np.uint64)
+        mult = (key * np.uint64(0x9E3779B97F4A7C15)) >> np.uint64(40)
+        sids[:, l] = ((mult + rank * np.uint64(2 * (l + 1) + 1)) % np.uint64(V)).astype(np.int64)
+        key = key * np.uint64(V + 1) + sids[:, l].astype(np.uint64) + np.uint64(1)
+    sids = np.unique(sids, axis=0)
+    n = sids.shape[0]
+    # ads and their matchers
+    arng = _rng(seed, "ads")
+    n_ads = np.minimum(1 + arng.geometric(0.7, size=n) - 1, 11)
+    ad_sid = np.repeat(np.arange(n), n_ads)
+    A = ad_sid.shape[0]
+    bm = np.zeros((A, GTM_W_BM), dtype=np.uint64)
+    base = 0
+    for size in GTM_ATTRS:
+        any_all = arng.random(A) < 0.5
+        rows = np.nonzero(any_all)[0]
+        for v in range(size):
+            _set_bits(bm, rows, np.full(rows.shape, base + v))
+        rows = np.nonzero(~any_all)[0]
+        cnt = arng.integers(1, 6, size=rows.shape[0])
+        rr = np.repeat(rows, cnt)
+        _set_bits(bm, rr, base + arng.integers(0, size, size=rr.shape[0]))
+        base += size
+    bl = np.zeros((A, GTM_W_BL), dtype=np.uint64)
+    any_loc = arng.random(A) < 0.4
+    bl[any_loc] = np.uint64(0xFFFFFFFFFFFFFFFF)
+    rows = np.nonzero(~any_loc)[0]
+    cnt = arng.integers(1, 9, size=rows.shape[0])
+    rr = np.repeat(rows, cnt)
+    bits = _bloom_bits(arng.integers(0, GTM_LOCS, size=rr.shape[0]))
+    for j in range(3):
+        _set_bits(bl, rr, bits[:, j])
+    # trie levels: node ids in level order, root = 0
+    level_ids, level_first = [], [1]
+    inv_prev = np.zeros(n, dtype=np.int64)          # level-0 prefix id of every SID (the root)
+    parent_of, token_of = [], []
+    for l in range(sid_len):
+        keys = np.concatenate([inv_prev[:, None], sids[:, l:l + 1]], axis=1)
+        uniq, inv = np.unique(keys, axis=0, return_inverse=True)
+        inv = inv.reshape(-1)
+        first = level_first[-1]
+        parent_of.append(uniq[:, 0] + (0 if l == 0 else level_first[-2]))
+        token_of.append(uniq[:, 1])
+        level_ids.append(first + inv)
+        level_first.append(first + uniq.shape[0])
+        inv_prev = inv
+    num_nodes = level_first[-1]
+    # node matchers: full SIDs OR their ads, then each level ORs its children
+    node_bm = np.zeros((num_nodes, GTM_W_BM), dtype=np.uint64)
+    node_bl = np.zeros((num_nodes, GTM_W_BL), dtype=np.uint64)
+    leaf = level_ids[-1][ad_sid]
+    np.bitwise_or.at(node_bm, leaf, bm)
+    np.bitwise_or.at(node_bl, leaf, bl)
+    for l in range(sid_len - 1, 0, -1):
+        kids = np.arange(level_first[l], level_first[l + 1])
+        np.bitwise_or.at(node_bm, parent_of[l], node_bm[kids])
+        np.bitwise_or.at(node_bl, parent_of[l], node_bl[kids])
+    # CSR child entries, ordered by (parent, token)
+    child = np.arange(1, num_nodes)
+    par = np.concatenate(parent_of)
+    tok = np.concatenate(token_of)
+    order = np.lexsort((tok, par))
+    child, par, tok = child[order], par[order], tok[order]
+    offsets = np.zeros(num_nodes + 1, dtype=np.int64)
+    np.add.at(offsets, par + 1, 1)
+    offsets = np.cumsum(offsets)
+    bm_tab, bm_idx = np.unique(node_bm[child], axis=0, return_inverse=True)
+    bl_tab, bl_idx = np.unique(node_bl[child], axis=0, return_inverse=True)
+    return {"vocab": V, "sid_len": sid_len, "num_nodes": num_nodes, "level_first": level_first,
+            "node_offsets": offsets.astype(np.int32), "child_nodes": child.astype(np.int32),
+            "tokens": tok.astype(np.int16), "bitmask_index": bm_idx.reshape(-1).astype(np.int32),
+            "bloom_index": bl_idx.reshape(-1).astype(np.int32),
+            "bitmask_table": np.ascontiguousarray(bm_tab), "bloom_table": np.ascontiguousarray(bl_tab),
+            "sids": sids, "ad_sid": ad_sid, "ad_bitmask": bm, "ad_bloom": bl}
+
+
+def gtm_users(seed: int, B: int, L_max: int = 64) -> dict:
+    rng = _rng(seed, "users")
+    u = np.zeros((B, GTM_W_BM), dtype=np.uint64)
+    base = 0
+    for size in GTM_ATTRS:
+        _set_bits(u, np.arange(B), base + rng.integers(0, size, size=B))
+        base += size
+    few = rng.integers(1, min(8, L_max) + 1, size=B)
+    many = rng.integers(min(9, L_max), L_max + 1, size=B)
+    n_loc = np.where(rng.random(B) < 0.9, few, many)
+    bloom = np.zeros((B, L_max, GTM_W_BL), dtype=np.uint64)
+    for b in range(B):
+        bits = _bloom_bits(rng.integers(0, GTM_LOCS, size=int(n_loc[b])))
+        for j in range(3):
+            _set_bits(bloom[b], np.arange(int(n_loc[b])), bits[:, j])
+    return {"bitmask": u, "bloom": bloom, "n_loc": n_loc.astype(np.int32), "L_max": L_max}
+
+
+def gtm_beam_nodes(seed: int, index: dict, B: int, M: int, level: int) -> np.ndarray:
+    """Node id of every beam (row b*M + m): a level-``level`` trie node (root at 0)."""
+    lf = index["level_first"]
+    if level == 0:
+        return np.zeros(B * M, dtype=np.int32)
+    lo, hi = lf[level - 1], lf[level]
+    return _rng(seed, "beam_nodes", level).integers(lo, hi, size=B * M).astype(np.int32)
