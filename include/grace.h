@@ -20,6 +20,9 @@
  *   grace_beam_topk       per-request top-k that yields the next step's beams,
  *                         i.e. the parents the rearrangement consumes (Sec. 3.1,
  *                         Sec. 3.3);
+ *   grace_gtm_mask        decode-time constraint filter: constrained decoding on
+ *                         the SID trie and target matching (Sec. 6, App. A);
+ *   grace_trie_advance    the trie node each selected beam moves to (Sec. 6.4);
  *   grace_graph_*         capture of a sequence of these calls (a whole decode
  *                         loop) as one replayable HIP graph (Sec. 5).
  *
@@ -283,6 +286,88 @@ int64_t grace_beam_topk_workspace_bytes(int32_t B, int32_t M, int32_t V);
 int32_t grace_beam_topk(const float* cand, const float* row_max, int32_t B, int32_t M, int32_t V,
                         int32_t k, void* workspace, int64_t workspace_bytes, int32_t* parents,
                         int32_t* tokens, float* scores, void* stream);
+
+/*
+ * The CD + GTM index (Sec. 6.4, App. A): the SID trie in CSR form.  Node 0 is
+ * the root; node i's child entries are [node_offsets[i], node_offsets[i+1]).
+ * Entry e leads by token tokens[e] to node child_nodes[e]; its eligibility
+ * matchers are row bitmask_index[e] of bitmask_table and row bloom_index[e] of
+ * bloom_table (deduplicated tables of packed uint64 words).  Within a node's
+ * range tokens are distinct and ascending.  The struct lives in host memory;
+ * every pointer in it is a device pointer.
+ */
+typedef struct grace_gtm_index {
+  int32_t vocab;             /* |V|, 1..4096; tokens lie in [0, vocab)             */
+  int32_t num_nodes;         /* trie nodes (>= 1)                                  */
+  int32_t num_entries;       /* child entries (>= 0)                               */
+  int32_t bitmask_words;     /* W_bm, 1..8 words per bitmask row                   */
+  int32_t bloom_words;       /* W_bl, 1..4 words per Bloom row                     */
+  int32_t bitmask_rows;      /* rows of bitmask_table                              */
+  int32_t bloom_rows;        /* rows of bloom_table                                */
+  int32_t reserved;          /* must be 0                                          */
+  const int32_t* node_offsets;   /* int32 [num_nodes + 1]                          */
+  const int32_t* child_nodes;    /* int32 [num_entries]                            */
+  const int16_t* tokens;         /* int16 [num_entries]                            */
+  const int32_t* bitmask_index;  /* int32 [num_entries]                            */
+  const int32_t* bloom_index;    /* int32 [num_entries]                            */
+  const uint64_t* bitmask_table; /* uint64 [bitmask_rows, bitmask_words]           */
+  const uint64_t* bloom_table;   /* uint64 [bloom_rows, bloom_words]               */
+} grace_gtm_index;
+
+/*
+ * Request-side targeting attributes (Sec. 6.1, 6.2), one row per request.
+ * Host struct of device pointers.
+ */
+typedef struct grace_gtm_user {
+  int32_t max_locations;         /* L_max, 0..64                                   */
+  int32_t reserved;              /* must be 0                                      */
+  const uint64_t* bitmask;       /* uint64 [B, bitmask_words]: the user's bits     */
+  const uint64_t* bloom;         /* uint64 [B, max_locations, bloom_words]: one Bloom
+                                    row per user location                          */
+  const int32_t* num_locations;  /* int32 [B]; clamped into [0, max_locations]     */
+} grace_gtm_user;
+
+/*
+ * Decode-time constraint filter (Sec. 6; lookup of App. A).  Beam row
+ * r = b*M + m sits at trie node node_ids[r].  Token v is allowed for it when
+ *   CD:  some child entry e of the node has tokens[e] = v, and for that entry
+ *   GTM: (bitmask_table[bitmask_index[e]] & user.bitmask[b]) == user.bitmask[b]
+ *        over all words (every user attribute bit is present), and
+ *        (loc & bloom_table[bloom_index[e]]) == loc for at least one of the
+ *        request's num_locations[b] location rows loc (none: not allowed).
+ * Writes mask[r, w] for every word w < ceil(vocab/32): bit v % 32 of word v / 32
+ * set = v allowed, the filter grace_beam_scores consumes.  A negative node id
+ * is a dead beam (no token allowed).  A node id >= num_nodes, or a child entry
+ * whose token or matcher ids are out of range, allows nothing for it and sets
+ * *err_flag.
+ *
+ *   index, user   host structs (above)
+ *   node_ids      device int32 [B*M]
+ *   B, M          requests and beams per request; B*M*ceil(vocab/32) below 2^31
+ *   mask          device uint32 [B*M, ceil(vocab/32)], written; must not overlap inputs
+ *   err_flag      device int32 or NULL; set to 1 on bad index data, never cleared
+ *   stream        hipStream_t
+ */
+int32_t grace_gtm_mask(const grace_gtm_index* index, const grace_gtm_user* user,
+                       const int32_t* node_ids, int32_t B, int32_t M, uint32_t* mask,
+                       int32_t* err_flag, void* stream);
+
+/*
+ * Trie step after top-k (Sec. 6.4: the selected child node ids become the next
+ * step's node ids).  New beam i = b*k + j has parent p = parents[i] (request-
+ * local, [0, M_prev)) and token tokens[i]:
+ *   node_next[i] = child of node_prev[b*M_prev + p] reached by tokens[i],
+ *                  or -1 if that parent is dead or the token is not a child
+ *                  (a filtered candidate kept as a dead beam).
+ * A parent outside [0, M_prev) or a node id >= num_nodes gives -1 and sets *err_flag.
+ *
+ *   node_prev     device int32 [B*M_prev];  parents, tokens  device int32 [B*k]
+ *   node_next     device int32 [B*k], written; must not overlap the inputs
+ */
+int32_t grace_trie_advance(const grace_gtm_index* index, const int32_t* node_prev,
+                           const int32_t* parents, const int32_t* tokens, int32_t B,
+                           int32_t M_prev, int32_t k, int32_t* node_next, int32_t* err_flag,
+                           void* stream);
 
 /*
  * Graph capture (Sec. 5: the fixed-length decoding loop is captured as one

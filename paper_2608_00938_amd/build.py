@@ -14,7 +14,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 OBJ = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libgrace.so")
-SOURCES = ["grace_api.hip", "cross_attn.hip", "self_attn.hip", "beam.hip", "graph.hip"]
+SOURCES = ["grace_api.hip", "cross_attn.hip", "self_attn.hip", "beam.hip", "graph.hip", "gtm.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -269,3 +269,86 @@ int32_t grace_beam_topk(const float* cand, const float* row_max, int32_t B, int3
 }
 
 }  // extern "C"
+
+namespace {
+
+int32_t check_gtm_index(const grace_gtm_index* x) {
+  if (!x) return GRACE_ERR_NULL;
+  if (x->vocab < 1 || x->vocab > 4096 || x->num_nodes < 1 || x->num_entries < 0)
+    return GRACE_ERR_SHAPE;
+  if (x->bitmask_words < 1 || x->bitmask_words > 8 || x->bloom_words < 1 || x->bloom_words > 4)
+    return GRACE_ERR_UNSUPPORTED;
+  if (x->bitmask_rows < 0 || x->bloom_rows < 0 || x->reserved != 0) return GRACE_ERR_SHAPE;
+  if (!x->node_offsets || !x->child_nodes || !x->tokens || !x->bitmask_index || !x->bloom_index)
+    return GRACE_ERR_NULL;
+  if ((x->bitmask_rows > 0 && !x->bitmask_table) || (x->bloom_rows > 0 && !x->bloom_table))
+    return GRACE_ERR_NULL;
+  return GRACE_OK;
+}
+
+// Ranges of the index arrays (for alias checks against outputs).
+void gtm_index_ranges(const grace_gtm_index* x, Range* r) {
+  const int64_t E = x->num_entries;
+  r[0] = {x->node_offsets, ((int64_t)x->num_nodes + 1) * 4};
+  r[1] = {x->child_nodes, E * 4};
+  r[2] = {x->tokens, E * 2};
+  r[3] = {x->bitmask_index, E * 4};
+  r[4] = {x->bloom_index, E * 4};
+  r[5] = {x->bitmask_table, (int64_t)x->bitmask_rows * x->bitmask_words * 8};
+  r[6] = {x->bloom_table, (int64_t)x->bloom_rows * x->bloom_words * 8};
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t grace_gtm_mask(const grace_gtm_index* index, const grace_gtm_user* user,
+                       const int32_t* node_ids, int32_t B, int32_t M, uint32_t* mask,
+                       int32_t* err_flag, void* stream) {
+  int32_t st = check_gtm_index(index);
+  if (st != GRACE_OK) return st;
+  if (!user) return GRACE_ERR_NULL;
+  if (user->max_locations < 0 || user->max_locations > 64 || user->reserved != 0)
+    return GRACE_ERR_SHAPE;
+  if (B < 0 || M < 0) return GRACE_ERR_SHAPE;
+  const int64_t R = (int64_t)B * M, W = (index->vocab + 31) / 32;
+  if (R * W >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
+  if (R == 0) return GRACE_OK;
+  if (!node_ids || !mask || !user->bitmask || !user->num_locations) return GRACE_ERR_NULL;
+  if (user->max_locations > 0 && !user->bloom) return GRACE_ERR_NULL;
+  Range in[10];
+  gtm_index_ranges(index, in);
+  in[7] = {node_ids, R * 4};
+  in[8] = {user->bitmask, (int64_t)B * index->bitmask_words * 8};
+  in[9] = {user->bloom, (int64_t)B * user->max_locations * index->bloom_words * 8};
+  for (const Range& r : in)
+    if (overlaps(mask, R * W * 4, r.p, r.n)) return GRACE_ERR_ALIAS;
+  if (overlaps(mask, R * W * 4, user->num_locations, (int64_t)B * 4)) return GRACE_ERR_ALIAS;
+  return hip_status(grace::launch_gtm_mask(*index, *user, node_ids, (int32_t)R, M, mask, err_flag,
+                                           (hipStream_t)stream));
+}
+
+int32_t grace_trie_advance(const grace_gtm_index* index, const int32_t* node_prev,
+                           const int32_t* parents, const int32_t* tokens, int32_t B,
+                           int32_t M_prev, int32_t k, int32_t* node_next, int32_t* err_flag,
+                           void* stream) {
+  int32_t st = check_gtm_index(index);
+  if (st != GRACE_OK) return st;
+  if (B < 0 || M_prev < 1 || k < 0 || (int64_t)B * k >= ((int64_t)1 << 31) ||
+      (int64_t)B * M_prev >= ((int64_t)1 << 31))
+    return GRACE_ERR_SHAPE;
+  if ((int64_t)B * k == 0) return GRACE_OK;
+  if (!node_prev || !parents || !tokens || !node_next) return GRACE_ERR_NULL;
+  const int64_t n = (int64_t)B * k * 4;
+  Range in[10];
+  gtm_index_ranges(index, in);
+  in[7] = {node_prev, (int64_t)B * M_prev * 4};
+  in[8] = {parents, n};
+  in[9] = {tokens, n};
+  for (const Range& r : in)
+    if (overlaps(node_next, n, r.p, r.n)) return GRACE_ERR_ALIAS;
+  return hip_status(grace::launch_trie_advance(*index, node_prev, parents, tokens, B, M_prev, k,
+                                               node_next, err_flag, (hipStream_t)stream));
+}
+
+}  // extern "C"

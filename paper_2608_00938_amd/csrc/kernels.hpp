@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/grace.h"
+
 namespace grace {
 
 // Cross-attention, beam-as-query: grid over (request, head, beam tile).
@@ -47,5 +49,14 @@ hipError_t launch_beam_topk(const float* cand, const float* row_max, int32_t B, 
                             int32_t* tokens, float* scores, hipStream_t stream);
 size_t beam_topk_workspace_bytes(int32_t B, int32_t M, int32_t V);
 int32_t beam_topk_max_k();
+
+// CD + GTM filter words of every beam row; next trie node of every new beam.
+hipError_t launch_gtm_mask(const grace_gtm_index& index, const grace_gtm_user& user,
+                           const int32_t* node_ids, int32_t R, int32_t M, uint32_t* mask,
+                           int32_t* err_flag, hipStream_t stream);
+hipError_t launch_trie_advance(const grace_gtm_index& index, const int32_t* node_prev,
+                               const int32_t* parents, const int32_t* tokens, int32_t B,
+                               int32_t M_prev, int32_t k, int32_t* node_next, int32_t* err_flag,
+                               hipStream_t stream);
 
 }  // namespace grace

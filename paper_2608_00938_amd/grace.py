@@ -23,6 +23,25 @@ GRACE_OK, GRACE_ERR_NULL, GRACE_ERR_SHAPE, GRACE_ERR_UNSUPPORTED, GRACE_ERR_ALIA
 _DTYPE_CODE = {torch.float32: GRACE_F32, torch.bfloat16: GRACE_BF16}
 
 _c_int, _c_float, _c_void_p = ctypes.c_int32, ctypes.c_float, ctypes.c_void_p
+
+
+class GtmIndexC(ctypes.Structure):
+    """Mirror of ``grace_gtm_index``."""
+    _fields_ = [("vocab", ctypes.c_int32), ("num_nodes", ctypes.c_int32),
+                ("num_entries", ctypes.c_int32), ("bitmask_words", ctypes.c_int32),
+                ("bloom_words", ctypes.c_int32), ("bitmask_rows", ctypes.c_int32),
+                ("bloom_rows", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("node_offsets", ctypes.c_void_p), ("child_nodes", ctypes.c_void_p),
+                ("tokens", ctypes.c_void_p), ("bitmask_index", ctypes.c_void_p),
+                ("bloom_index", ctypes.c_void_p), ("bitmask_table", ctypes.c_void_p),
+                ("bloom_table", ctypes.c_void_p)]
+
+
+class GtmUserC(ctypes.Structure):
+    """Mirror of ``grace_gtm_user``."""
+    _fields_ = [("max_locations", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("bitmask", ctypes.c_void_p), ("bloom", ctypes.c_void_p),
+                ("num_locations", ctypes.c_void_p)]
 _SIGNATURES = {
     "grace_cross_attn": [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_int, _c_int, _c_int,
                          _c_int, _c_int, _c_float, _c_int, _c_void_p, _c_void_p],
@@ -45,6 +64,10 @@ _SIGNATURES = {
     "grace_beam_topk_workspace_bytes": [_c_int, _c_int, _c_int],
     "grace_beam_topk": [_c_void_p, _c_void_p, _c_int, _c_int, _c_int, _c_int, _c_void_p,
                         ctypes.c_int64, _c_void_p, _c_void_p, _c_void_p, _c_void_p],
+    "grace_gtm_mask": [ctypes.POINTER(GtmIndexC), ctypes.POINTER(GtmUserC), _c_void_p, _c_int,
+                       _c_int, _c_void_p, _c_void_p, _c_void_p],
+    "grace_trie_advance": [ctypes.POINTER(GtmIndexC), _c_void_p, _c_void_p, _c_void_p, _c_int,
+                           _c_int, _c_int, _c_void_p, _c_void_p, _c_void_p],
     "grace_graph_begin": [_c_void_p],
     "grace_graph_end": [_c_void_p, ctypes.POINTER(_c_void_p)],
     "grace_graph_launch": [_c_void_p, _c_void_p],
@@ -238,6 +261,74 @@ def grace_beam_topk(cand, B: int, M: int, k: int, row_max=None, parents=None, to
                                    _ptr(tokens), _ptr(scores), _stream(cand))
     _check(st, "grace_beam_topk")
     return parents, tokens, scores
+
+
+def _dev(a, dtype, device):
+    """numpy array -> contiguous device tensor (uint64 words travel as int64 bit patterns)."""
+    import numpy as np
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint64:
+        a = a.view(np.int64)
+    return torch.from_numpy(a).to(device=device, dtype=dtype)
+
+
+class GtmIndex:
+    """Device copy of a CD+GTM index (grace_gtm_index): CSR trie + matcher tables."""
+
+    def __init__(self, ix: dict, device="cuda"):
+        import numpy as np
+        self.vocab = int(ix["vocab"])
+        self.t = dict(
+            node_offsets=_dev(ix["node_offsets"].astype(np.int32), torch.int32, device),
+            child_nodes=_dev(ix["child_nodes"].astype(np.int32), torch.int32, device),
+            tokens=_dev(ix["tokens"].astype(np.int16), torch.int16, device),
+            bitmask_index=_dev(ix["bitmask_index"].astype(np.int32), torch.int32, device),
+            bloom_index=_dev(ix["bloom_index"].astype(np.int32), torch.int32, device),
+            bitmask_table=_dev(ix["bitmask_table"], torch.int64, device),
+            bloom_table=_dev(ix["bloom_table"], torch.int64, device))
+        bm, bl = ix["bitmask_table"], ix["bloom_table"]
+        self.c = GtmIndexC(self.vocab, ix["node_offsets"].shape[0] - 1, ix["tokens"].shape[0],
+                           bm.shape[1], bl.shape[1], bm.shape[0], bl.shape[0], 0,
+                           *(_ptr(self.t[k]) for k in ("node_offsets", "child_nodes", "tokens",
+                                                        "bitmask_index", "bloom_index",
+                                                        "bitmask_table", "bloom_table")))
+
+
+class GtmUsers:
+    """Device copy of the requests' targeting attributes (grace_gtm_user)."""
+
+    def __init__(self, us: dict, device="cuda"):
+        self.t = dict(bitmask=_dev(us["bitmask"], torch.int64, device),
+                      bloom=_dev(us["bloom"], torch.int64, device),
+                      n_loc=_dev(us["n_loc"], torch.int32, device))
+        self.c = GtmUserC(int(us["bloom"].shape[1]), 0, _ptr(self.t["bitmask"]),
+                          _ptr(self.t["bloom"]), _ptr(self.t["n_loc"]))
+
+
+def grace_gtm_mask(index: GtmIndex, users: GtmUsers, node_ids, B: int, M: int, mask=None,
+                   err_flag=None):
+    """Constraint filter words (int32 view of uint32) [B*M, ceil(V/32)] of the beams at node_ids."""
+    _contig(node_ids, mask)
+    W = (index.vocab + 31) // 32
+    if mask is None:
+        mask = torch.empty((B * M, W), dtype=torch.int32, device=node_ids.device)
+    st = library().grace_gtm_mask(ctypes.byref(index.c), ctypes.byref(users.c), _ptr(node_ids), B, M,
+                                  _ptr(mask), _ptr(err_flag), _stream(node_ids))
+    _check(st, "grace_gtm_mask")
+    return mask
+
+
+def grace_trie_advance(index: GtmIndex, node_prev, parents, tokens, B: int, M_prev: int, k: int,
+                       node_next=None, err_flag=None):
+    """Trie node of every new beam [B*k] from its parent's node and its token."""
+    _contig(node_prev, parents, tokens, node_next)
+    if node_next is None:
+        node_next = torch.empty((B * k,), dtype=torch.int32, device=node_prev.device)
+    st = library().grace_trie_advance(ctypes.byref(index.c), _ptr(node_prev), _ptr(parents),
+                                      _ptr(tokens), B, M_prev, k, _ptr(node_next), _ptr(err_flag),
+                                      _stream(node_prev))
+    _check(st, "grace_trie_advance")
+    return node_next
 
 
 class Graph:

@@ -31,7 +31,7 @@ def test_header_declares_the_boundary():
     for n in ("grace_cross_attn", "grace_kv_append", "grace_self_attn_step",
               "grace_self_attn_step_fused", "grace_self_attn_step_fused_dyn",
               "grace_beam_scores", "grace_beam_topk", "grace_beam_topk_max_k",
-              "grace_beam_topk_workspace_bytes"):
+              "grace_beam_topk_workspace_bytes", "grace_gtm_mask", "grace_trie_advance"):
         assert n in names
 
 
@@ -236,6 +236,62 @@ def test_beam_topk_max_k_and_workspace():
     assert lib.grace_beam_topk_workspace_bytes(2, 0, 64) == -1
     small, big = lib.grace_beam_topk_workspace_bytes(1, 8, 64), lib.grace_beam_topk_workspace_bytes(64, 4096, 512)
     assert 0 < small < big < (128 << 20)
+
+
+def _gtm_index(**kw):
+    a = dict(vocab=512, num_nodes=10, num_entries=9, bitmask_words=7, bloom_words=4, bitmask_rows=5,
+             bloom_rows=5, reserved=0, node_offsets=0x100000, child_nodes=0x200000, tokens=0x300000,
+             bitmask_index=0x400000, bloom_index=0x500000, bitmask_table=0x600000,
+             bloom_table=0x700000)
+    a.update(kw)
+    return G.GtmIndexC(*[a[f] for f, _ in G.GtmIndexC._fields_])
+
+
+def _gtm_user(**kw):
+    a = dict(max_locations=8, reserved=0, bitmask=0x800000, bloom=0x900000, num_locations=0xA00000)
+    a.update(kw)
+    return G.GtmUserC(*[a[f] for f, _ in G.GtmUserC._fields_])
+
+
+@pytest.mark.parametrize("ix,us,extra,status", [
+    (dict(vocab=0), {}, {}, G.GRACE_ERR_SHAPE), (dict(vocab=5000), {}, {}, G.GRACE_ERR_SHAPE),
+    (dict(bitmask_words=9), {}, {}, G.GRACE_ERR_UNSUPPORTED),
+    (dict(bloom_words=5), {}, {}, G.GRACE_ERR_UNSUPPORTED),
+    (dict(reserved=1), {}, {}, G.GRACE_ERR_SHAPE), (dict(num_nodes=0), {}, {}, G.GRACE_ERR_SHAPE),
+    (dict(tokens=0), {}, {}, G.GRACE_ERR_NULL), (dict(bloom_table=0), {}, {}, G.GRACE_ERR_NULL),
+    ({}, dict(max_locations=65), {}, G.GRACE_ERR_SHAPE), ({}, dict(bitmask=0), {}, G.GRACE_ERR_NULL),
+    ({}, {}, dict(mask=None), G.GRACE_ERR_NULL),
+    ({}, {}, dict(mask=ctypes.c_void_p(0x300000 + 2)), G.GRACE_ERR_ALIAS),   # over tokens
+    ({}, {}, dict(mask=ctypes.c_void_p(0xB00000 - 8)), G.GRACE_ERR_ALIAS),   # over node ids
+    ({}, {}, dict(B=0), G.GRACE_OK),
+])
+def test_gtm_mask_rejects(ix, us, extra, status):
+    a = dict(nodes=ctypes.c_void_p(0xB00000), B=2, M=4, mask=ctypes.c_void_p(0xC00000))
+    a.update(extra)
+    idx, usr = _gtm_index(**ix), _gtm_user(**us)
+    assert G.library().grace_gtm_mask(ctypes.byref(idx), ctypes.byref(usr), a["nodes"], a["B"], a["M"],
+                                      a["mask"], None, None) == status
+
+
+def test_gtm_mask_null_structs():
+    lib = G.library()
+    assert lib.grace_gtm_mask(None, ctypes.byref(_gtm_user()), P, 1, 1, P2, None, None) == G.GRACE_ERR_NULL
+    assert lib.grace_gtm_mask(ctypes.byref(_gtm_index()), None, P, 1, 1, P2, None, None) == G.GRACE_ERR_NULL
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(Mp=0), G.GRACE_ERR_SHAPE), (dict(k=-1), G.GRACE_ERR_SHAPE),
+    (dict(par=None), G.GRACE_ERR_NULL),
+    (dict(out=ctypes.c_void_p(0xD00000 + 4)), G.GRACE_ERR_ALIAS),     # over parents
+    (dict(k=0), G.GRACE_OK),
+])
+def test_trie_advance_rejects(kw, status):
+    a = dict(prev=ctypes.c_void_p(0xC00000), par=ctypes.c_void_p(0xD00000), tok=ctypes.c_void_p(0xE00000),
+             B=2, Mp=4, k=3, out=ctypes.c_void_p(0xF00000))
+    a.update(kw)
+    idx = _gtm_index()
+    assert G.library().grace_trie_advance(ctypes.byref(idx), a["prev"], a["par"], a["tok"], a["B"], a["Mp"],
+                                          a["k"], a["out"], None, None) == status
 
 
 def test_graph_api_rejects_null():
