@@ -166,6 +166,43 @@ def bench_beam_step(wl, dev, reps=10):
             "note": "side measurement, not part of value"}
 
 
+def bench_gtm(wl, dev, n_sids=300_000, reps=10):
+    """Side measurement: CD+GTM filter of every beam at the workload's shape on a
+    synthetic CSR trie (W_bm = 7, W_bl = 4, 1-64 user locations), beams at trie
+    level 2 and 3, and the trie step of k = M new beams."""
+    import torch
+    from paper_2608_00938_amd import grace as G
+    from paper_2608_00938_amd import workloads as W
+    ix, us = W.gtm_index(0, n_sids), W.gtm_users(0, wl.B)
+    gi, gu = G.GtmIndex(ix, dev), G.GtmUsers(us, dev)
+    out = {"index": f"{ix['num_nodes']} nodes, {ix['tokens'].shape[0]} child entries",
+           "beams": wl.R, "note": "side measurement, not part of value"}
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for level in (2, 3):
+        nodes = torch.from_numpy(W.gtm_beam_nodes(1, ix, wl.B, wl.M, level)).to(dev)
+        mask = torch.empty((wl.R, (W.VOCAB + 31) // 32), dtype=torch.int32, device=dev)
+        for _ in range(3):
+            G.grace_gtm_mask(gi, gu, nodes, wl.B, wl.M, mask=mask)
+        e0.record()
+        for _ in range(reps):
+            G.grace_gtm_mask(gi, gu, nodes, wl.B, wl.M, mask=mask)
+        e1.record()
+        torch.cuda.synchronize()
+        out[f"mask_level{level}_us"] = round(e0.elapsed_time(e1) / reps * 1e3, 1)
+    par = torch.from_numpy(W.parents(wl, 1)).to(dev)
+    tok = torch.zeros(wl.R, dtype=torch.int32, device=dev)
+    nxt = torch.empty(wl.R, dtype=torch.int32, device=dev)
+    for _ in range(3):
+        G.grace_trie_advance(gi, nodes, par, tok, wl.B, wl.M, wl.M, node_next=nxt)
+    e0.record()
+    for _ in range(reps):
+        G.grace_trie_advance(gi, nodes, par, tok, wl.B, wl.M, wl.M, node_next=nxt)
+    e1.record()
+    torch.cuda.synchronize()
+    out["trie_advance_us"] = round(e0.elapsed_time(e1) / reps * 1e3, 1)
+    return out
+
+
 def bench_decode_loop(dev, name="bf16_b8_m256", layers=3, reps=20):
     """Side measurement: a whole decode loop (layers x steps of cross-attention and
     fused paged self-attention, score update and top-k feeding the next step)
@@ -391,6 +428,7 @@ def main():
         torch.cuda.empty_cache()
         result["beam_step"] = bench_beam_step(wl, dev)
         result["decode_loop_graph"] = bench_decode_loop(dev)
+        result["gtm_filter"] = bench_gtm(wl, dev)
     if not args.no_cpu_baseline:
         log("timing the oracle on host cores ...")
         result["cpu_baseline"] = cpu_baseline(wl, inp, parents_np)

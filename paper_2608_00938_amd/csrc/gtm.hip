@@ -1,13 +1,12 @@
 // Decode-time constraint filter (CD + GTM) and trie step (GRACE, Sec. 6,
 // App. A) for gfx950.
 //
-// gtm_mask: one wave per beam row.  The row's request-side matchers (packed
-//   attribute bitmask, one Bloom row per user location) are the same for every
-//   lane of the wave, so they are loaded once per wave; the lanes split the
-//   beam's child-entry range (CSR), test the bitmask matcher first (stopping at
-//   the first word that misses a user bit), then the Bloom matcher (stopping at
-//   the first location it contains), and OR the surviving tokens into the row's
-//   filter words in LDS, which the wave then stores whole.
+// gtm_mask: 16 lanes per beam row.  The lanes split the beam's child-entry
+//   range (CSR), test the bitmask matcher first (stopping at the first word
+//   that misses a user bit), then the Bloom matcher (stopping at the first
+//   location it contains), and OR the surviving tokens into the row's filter
+//   words in LDS, which they then store whole.  The request-side matchers are
+//   shared by the beams of a request and stay in cache.
 // trie_advance: one lane per new beam: binary search of its token among the
 //   parent node's child tokens (ascending within a node's range).
 #include "common.hpp"
@@ -37,14 +36,22 @@ struct UserDev {
   int32_t lmax;
 };
 
+// A beam row is handled by kLanesPerBeam consecutive lanes (four beams per
+// wave): at the deeper trie levels a node has a handful of children, and more
+// beams per wave keep more of the dependent lookups (node -> range -> entries
+// -> matcher rows) in flight.
+constexpr int kLanesPerBeam = 16;
+constexpr int kBeamsPerBlock = kGtmThreads / kLanesPerBeam;
+
 __global__ void __launch_bounds__(kGtmThreads)
 gtm_mask_kernel(GtmDev ix, UserDev us, const int32_t* __restrict__ node_ids, int32_t R, int32_t M,
                 uint32_t* __restrict__ mask, int32_t* __restrict__ err_flag) {
-  __shared__ uint32_t words[kGtmThreads / 64][kGtmMaxWords];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int32_t r = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * (kGtmThreads / 64) + w);
+  __shared__ uint32_t words[kBeamsPerBlock][kGtmMaxWords];
+  const int sub = threadIdx.x % kLanesPerBeam, slot = threadIdx.x / kLanesPerBeam;
+  const int32_t r = (int32_t)blockIdx.x * kBeamsPerBlock + slot;
   const int W = (ix.V + 31) >> 5;
-  for (int i = lane; i < W; i += 64) words[w][i] = 0u;
+  for (int i = sub; i < W; i += kLanesPerBeam) words[slot][i] = 0u;
+  __syncthreads();
   bool bad = false;
   if (r < R) {
     const int32_t node = node_ids[r];
@@ -59,7 +66,7 @@ gtm_mask_kernel(GtmDev ix, UserDev us, const int32_t* __restrict__ node_ids, int
       int32_t e0 = ix.off[node], e1 = ix.off[node + 1];
       e0 = e0 < 0 ? 0 : (e0 > ix.entries ? ix.entries : e0);
       e1 = e1 < e0 ? e0 : (e1 > ix.entries ? ix.entries : e1);
-      for (int32_t e = e0 + lane; e < e1; e += 64) {
+      for (int32_t e = e0 + sub; e < e1; e += kLanesPerBeam) {
         const int32_t v = ix.tok[e], bi = ix.bmi[e], li = ix.bli[e];
         if (v < 0 || v >= ix.V || bi < 0 || bi >= ix.bm_rows || li < 0 || li >= ix.bl_rows) {
           bad = true;
@@ -91,7 +98,7 @@ gtm_mask_kernel(GtmDev ix, UserDev us, const int32_t* __restrict__ node_ids, int
           }
           found = in;
         }
-        if (found) atomicOr(&words[w][v >> 5], 1u << (v & 31));
+        if (found) atomicOr(&words[slot][v >> 5], 1u << (v & 31));
       }
     } else if (node >= ix.nodes) {
       bad = true;   // negative ids are dead beams; ids past the trie are errors
@@ -99,7 +106,7 @@ gtm_mask_kernel(GtmDev ix, UserDev us, const int32_t* __restrict__ node_ids, int
   }
   __syncthreads();
   if (r < R)
-    for (int i = lane; i < W; i += 64) mask[(int64_t)r * W + i] = words[w][i];
+    for (int i = sub; i < W; i += kLanesPerBeam) mask[(int64_t)r * W + i] = words[slot][i];
   if (bad && err_flag) *err_flag = 1;
 }
 
@@ -144,7 +151,7 @@ hipError_t launch_gtm_mask(const grace_gtm_index& index, const grace_gtm_user& u
                            const int32_t* node_ids, int32_t R, int32_t M, uint32_t* mask,
                            int32_t* err_flag, hipStream_t stream) {
   const UserDev us{user.bitmask, user.bloom, user.num_locations, user.max_locations};
-  const int64_t blocks = ((int64_t)R + kGtmThreads / 64 - 1) / (kGtmThreads / 64);
+  const int64_t blocks = ((int64_t)R + kBeamsPerBlock - 1) / kBeamsPerBlock;
   hipLaunchKernelGGL(gtm_mask_kernel, dim3((unsigned)blocks), dim3(kGtmThreads), 0, stream,
                      to_dev(index), us, node_ids, R, M, mask, err_flag);
   return hipGetLastError();
