@@ -3,9 +3,10 @@
 Per step t (beam width M_t per request) and decoder layer l:
 cross-attention of the beams over the request's encoder K/V (Sec. 5.1), then
 the fused paged append + self-attention (Sec. 5.2, Sec. 5.3) whose parents are
-the previous step's top-k output.  After the layers, the beam score update
-(Sec. 3.1) and top-k with k = M_{t+1} (Sec. 3.3) produce the next step's
-parents and prefix scores on the device, so the whole loop runs without a host
+the previous step's top-k output.  After the layers, the constraint filter
+(CD + GTM, Sec. 6) of the beams' trie nodes, the beam score update (Sec. 3.1)
+and top-k with k = M_{t+1} (Sec. 3.3) produce the next step's parents, prefix
+scores and trie nodes on the device, so the whole loop runs without a host
 round trip and is recorded as one graph (Sec. 5).
 
 Inputs the model would compute (per-step queries, the current token's k/v and
@@ -25,10 +26,12 @@ from . import grace as G
 class DecodeLoop:
     def __init__(self, B: int, widths, H: int, d: int, V: int, layers: int, enc_k, enc_v,
                  enc_off, step_inputs, logits, masks=None, k_final: int | None = None,
-                 scale: float | None = None):
+                 scale: float | None = None, gtm=None):
         """widths: beams per request at each step (M_0, ..., M_{T-1}).
         step_inputs[l][t]: dict(q_cross, q_self, k_new, v_new), each [B*M_t, H, d].
         logits[t]: [B*M_t, V]; masks[t]: packed filter words (int32 [B*M_t, ceil(V/32)]) or None.
+        gtm: (GtmIndex, GtmUsers) to compute the filter of every step from the
+        beams' trie nodes instead (masks is then ignored); beams start at the root.
         The top-k of step t keeps M_{t+1} beams; the last keeps k_final (default M_{T-1})."""
         self.B, self.widths, self.H, self.d, self.V, self.layers = B, tuple(widths), H, d, V, layers
         self.T = len(self.widths)
@@ -52,6 +55,13 @@ class DecodeLoop:
         self.scores = [torch.empty((B, k), dtype=torch.float32, device=dev) for k in self.k_out]
         ws = max(G.grace_beam_topk_workspace_bytes(B, M, V) for M in self.widths)
         self.workspace = torch.empty((max(ws, 8),), dtype=torch.uint8, device=dev)
+        self.gtm = gtm
+        if gtm is not None:
+            W = (V + 31) // 32
+            self.masks = [torch.empty((B * M, W), dtype=torch.int32, device=dev) for M in self.widths]
+            self.nodes = [torch.zeros((B * self.widths[0],), dtype=torch.int32, device=dev)] + \
+                [torch.empty((B * k,), dtype=torch.int32, device=dev) for k in self.k_out]
+            self.gtm_err = torch.zeros(1, dtype=torch.int32, device=dev)
 
     def run(self):
         """Enqueue the whole loop on the current stream."""
@@ -66,11 +76,19 @@ class DecodeLoop:
                 self.caches[l].append_attend_dyn(t, x["q_self"], x["k_new"], x["v_new"], par,
                                                  M_prev, M, self.scale, out=self.x_self[l][t])
             prev = self.prev0 if t == 0 else self.scores[t - 1].view(-1)
+            if self.gtm is not None:
+                index, users = self.gtm
+                G.grace_gtm_mask(index, users, self.nodes[t], B, M, mask=self.masks[t],
+                                 err_flag=self.gtm_err)
             G.grace_beam_scores(self.logits[t], prev, self.masks[t], cand=self.cand[t],
                                 row_max=self.row_max[t])
             G.grace_beam_topk(self.cand[t], B, M, self.k_out[t], row_max=self.row_max[t],
                               parents=self.parents[t], tokens=self.tokens[t],
                               scores=self.scores[t], workspace=self.workspace)
+            if self.gtm is not None:
+                G.grace_trie_advance(self.gtm[0], self.nodes[t], self.parents[t].view(-1),
+                                     self.tokens[t].view(-1), B, M, self.k_out[t],
+                                     node_next=self.nodes[t + 1], err_flag=self.gtm_err)
 
     def capture(self, stream) -> "G.Graph":
         """Record run() on ``stream`` (not the null stream) as one graph."""

@@ -26,7 +26,8 @@ def _log(msg):
     sys.stdout.flush()
 
 
-def _make_loop(dev, B=2, widths=(1, 8, 16, 16), H=2, d=64, V=64, layers=2, L=24, seed=31):
+def _make_loop(dev, B=2, widths=(1, 8, 16, 16), H=2, d=64, V=64, layers=2, L=24, seed=31,
+               gtm=None):
     wl = W.custom(dtype="bf16", B=B, M=max(widths), H=H, d=d, steps=len(widths), L=L)
     inp = W.DecodeInputs(wl, seed, dev)
     ek, ev = inp.enc_kv
@@ -42,8 +43,14 @@ def _make_loop(dev, B=2, widths=(1, 8, 16, 16), H=2, d=64, V=64, layers=2, L=24,
     logits = [W.beam_logits(seed, t, B * M, V, "bf16", dev) for t, M in enumerate(widths)]
     masks = [torch.from_numpy(W.beam_mask(seed, t, B * M, V, keep=0.7).view(np.int32)).to(dev)
              for t, M in enumerate(widths)]
-    loop = D.DecodeLoop(B, widths, H, d, V, layers, ek, ev, off, step_inputs, logits, masks)
+    loop = D.DecodeLoop(B, widths, H, d, V, layers, ek, ev, off, step_inputs, logits, masks,
+                        gtm=gtm)
     return loop, inp
+
+
+def _gtm(dev, B, seed=41):
+    ix = W.gtm_index(seed, 20000)
+    return ix, (G.GtmIndex(ix, dev), G.GtmUsers(W.gtm_users(seed, B, L_max=16), dev))
 
 
 def _snapshot(loop):
@@ -51,6 +58,8 @@ def _snapshot(loop):
     for l in range(loop.layers):
         outs += [x.clone() for x in loop.x_cross[l]] + [x.clone() for x in loop.x_self[l]]
     outs += [x.clone() for x in loop.parents + loop.tokens + loop.scores]
+    if loop.gtm is not None:
+        outs += [x.clone() for x in loop.masks + loop.nodes[1:]]
     return outs + [x.clone() for x in _written_slabs(loop)]
 
 
@@ -68,11 +77,15 @@ def _current(loop):
     for l in range(loop.layers):
         outs += list(loop.x_cross[l]) + list(loop.x_self[l])
     outs += list(loop.parents + loop.tokens + loop.scores)
+    if loop.gtm is not None:
+        outs += list(loop.masks + loop.nodes[1:])
     return outs + _written_slabs(loop)
 
 
-def test_decode_loop_graph_replays_match_eager(gpu):
-    loop, _ = _make_loop(gpu)
+@pytest.mark.parametrize("with_gtm", [False, True], ids=["given_masks", "cd_gtm"])
+def test_decode_loop_graph_replays_match_eager(gpu, with_gtm):
+    gtm = _gtm(gpu, 2)[1] if with_gtm else None
+    loop, _ = _make_loop(gpu, V=512 if with_gtm else 64, gtm=gtm)
     stream = torch.cuda.Stream()
     with torch.cuda.stream(stream):
         loop.run()
@@ -123,3 +136,37 @@ def test_decode_loop_wiring(gpu):
 def test_graph_capture_on_null_stream_is_refused(gpu):
     with pytest.raises(G.GraceError):
         G.capture(lambda: None, torch.cuda.default_stream())
+
+
+def test_decode_loop_with_filter_follows_the_trie(gpu):
+    """With the CD+GTM filter in the loop, every finite beam's token sequence is a
+    prefix of a valid SID (its node is real), and its trie node is the walk of
+    its tokens (reconstructed from parents on the host)."""
+    B = 2
+    ix, gtm = _gtm(gpu, B)
+    loop, _ = _make_loop(gpu, V=512, gtm=gtm)
+    loop.run()
+    torch.cuda.synchronize()
+    assert int(loop.gtm_err.item()) == 0
+    off, tok, child = ix["node_offsets"], ix["tokens"], ix["child_nodes"]
+    T = loop.T
+    par = [p.cpu().numpy() for p in loop.parents]
+    toks = [t.cpu().numpy() for t in loop.tokens]
+    sc = loop.scores[-1].cpu().numpy()
+    node_last = loop.nodes[T].cpu().numpy().reshape(B, -1)
+    for b in range(B):
+        for j in range(sc.shape[1]):
+            if not np.isfinite(sc[b, j]):
+                continue
+            seq, jj = [], j
+            for t in range(T - 1, -1, -1):          # walk back through the parents
+                seq.append(int(toks[t][b, jj]))
+                jj = int(par[t][b, jj])
+            seq.reverse()
+            node = 0
+            for v in seq:                            # walk down the trie
+                rng = range(off[node], off[node + 1])
+                hit = [e for e in rng if tok[e] == v]
+                assert hit, (b, j, seq)
+                node = int(child[hit[0]])
+            assert node == node_last[b, j]
