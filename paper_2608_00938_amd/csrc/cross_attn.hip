@@ -542,8 +542,8 @@ cross_attn_bf16_dual_kernel(const uint16_t* __restrict__ q, const uint16_t* __re
 
   // Softmax bookkeeping of tile t on S(t)^T: mask the keys past L, take each
   // beam's maximum and, when a beam needs it (rare), move its shift.
-  float alpha[C::kMB];
-  auto softmax_shift = [&](int32_t t) __attribute__((always_inline)) -> bool {
+  // Keys past L in the last, partial tile get weight 0.
+  auto mask_tail = [&](int32_t t) __attribute__((always_inline)) {
     const int32_t t0 = t * C::kBlockN;
     if (t0 + C::kBlockN > L) {
 #pragma unroll
@@ -557,6 +557,10 @@ cross_attn_bf16_dual_kernel(const uint16_t* __restrict__ q, const uint16_t* __re
           }
         }
     }
+  };
+  float alpha[C::kMB];
+  auto softmax_shift = [&](int32_t t) __attribute__((always_inline)) -> bool {
+    mask_tail(t);
     float mx[C::kMB];
     bool any = false;
 #pragma unroll
@@ -611,13 +615,6 @@ cross_attn_bf16_dual_kernel(const uint16_t* __restrict__ q, const uint16_t* __re
         for (int r = 0; r < 16; ++r) o[db][mb][r] *= alpha[mb];
     }
   };
-  auto s_tile = [&](int32_t t) __attribute__((always_inline)) {
-    const char* kbp = kbuf0 + (t % C::kNBuf) * C::kTileBytes;
-    if (biased)
-      qk(kbp, std::true_type{});
-    else
-      qk(kbp, std::false_type{});
-  };
   // Loads for tiles ahead of t, then (after this tile's work) the wait for
   // K(t+1) and V(t) and the barrier that publishes them.
   auto prefetch = [&](int32_t t) __attribute__((always_inline)) -> int {
@@ -631,33 +628,109 @@ cross_attn_bf16_dual_kernel(const uint16_t* __restrict__ q, const uint16_t* __re
     lds_barrier();
   };
 
-  // Tile t: S(t)^T on the matrix core; then the softmax of tile t on the VALU
-  // with the MFMAs of O += V(t-1)^T P(t-1)^T interleaved into its exp/pack
-  // stream, so one wave keeps both pipes busy.  Tile 0 has no P before it and
-  // the last P is accumulated after the loop.
-  if (n > 0) {
-    const int issued = prefetch(0);
-    if (active) {
-      s_tile(0);
-      softmax_shift(0);   // O and the row sums are still zero: no rescale
+  // One pass over the request's tokens.  Tile t: S(t)^T on the matrix core;
+  // then the softmax of tile t on the VALU with the MFMAs of
+  // O += V(t-1)^T P(t-1)^T interleaved into its exp/pack stream, so one wave
+  // keeps both pipes busy.  Tile 0 has no P before it and the last P is
+  // accumulated after the loop.
+  //   fast pass (SAFE = false): the exponent shift stays 0 and no maximum is
+  //     taken; the result is kept only if every beam's row sum lands in
+  //     [2^-100, 2^64] and its outputs are finite (no overflow, no lost
+  //     precision to underflow);
+  //   safe pass (SAFE = true): the bookkeeping of the exponent shift described
+  //     above, valid for any input.  Run by the whole workgroup when any of its
+  //     beams failed the fast pass's check.
+  auto run_pass = [&](auto safe) __attribute__((always_inline)) {
+    constexpr bool SAFE = decltype(safe)::value;
+    auto s_tile = [&](int32_t t) __attribute__((always_inline)) {
+      const char* kbp = kbuf0 + (t % C::kNBuf) * C::kTileBytes;
+      if (SAFE && biased)
+        qk(kbp, std::true_type{});
+      else
+        qk(kbp, std::false_type{});
+    };
+    if (n > 0) {
+      const int issued = prefetch(0);
+      if (active) {
+        s_tile(0);
+        if constexpr (SAFE)
+          softmax_shift(0);   // O and the row sums are still zero: no rescale
+        else
+          mask_tail(0);
 #pragma unroll
-      for (int kc = 0; kc < C::kKC; ++kc)
+        for (int kc = 0; kc < C::kKC; ++kc)
 #pragma unroll
-        for (int mb = 0; mb < C::kMB; ++mb) exp_chunk(kc, mb);
+          for (int mb = 0; mb < C::kMB; ++mb) exp_chunk(kc, mb);
+      }
+      publish(issued);
     }
-    publish(issued);
-  }
-  for (int32_t t = 1; t < n; ++t) {
-    const int issued = prefetch(t);
-    if (active) {
-      s_tile(t);
-      const bool moved = softmax_shift(t);
-      pv_exp_tile(t - 1);
-      if (__builtin_expect(moved, 0)) rescale_after();
+    for (int32_t t = 1; t < n; ++t) {
+      const int issued = prefetch(t);
+      if (active) {
+        s_tile(t);
+        bool moved = false;
+        if constexpr (SAFE)
+          moved = softmax_shift(t);
+        else
+          mask_tail(t);
+        pv_exp_tile(t - 1);
+        if (SAFE && __builtin_expect(moved, 0)) rescale_after();
+      }
+      publish(issued);
     }
-    publish(issued);
+    if (active && n > 0) pv_tile(n - 1);
+  };
+
+  run_pass(std::false_type{});
+
+  // Keep the fast pass only if every beam of the workgroup passes the check.
+  {
+    bool bad = false;
+    if (active && n > 0) {
+#pragma unroll
+      for (int mb = 0; mb < C::kMB; ++mb) {
+        const float l = lsum[2 * mb], l2 = lsum[2 * mb + 1];   // lanes 0-15 hold the sums
+        if ((lane & 15) == lane)
+          bad |= !(l >= 0x1p-100f && l <= 0x1p64f) || !(l2 >= 0x1p-100f && l2 <= 0x1p64f);
+        float chk = 0.f;
+#pragma unroll
+        for (int db = 0; db < C::kDB; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) chk = __builtin_fmaf(o[db][mb][r], 0.f, chk);
+        bad |= chk != 0.f;   // inf * 0 and NaN * 0 are NaN
+      }
+    }
+    // One vote word per wave in K buffer 2: no wave reads K after the last
+    // tile's barrier, and the buffer is next written after the rerun's
+    // prologue barrier (K(2)), by which time every wave has read the votes.
+    // (An extra __shared__ word would push two workgroups past the CU's LDS.)
+    int32_t* votes = (int32_t*)(kbuf0 + 2 * C::kTileBytes);
+    const bool wave_bad = __any(bad);
+    if (lane == 0) votes[wave] = wave_bad ? 1 : 0;
+    lds_barrier();
+    bool rerun = false;
+#pragma unroll
+    for (int w = 0; w < C::kWaves; ++w) rerun |= votes[w] != 0;
+    if (rerun) {
+      // rare: the whole workgroup redoes the tokens with the exponent shift
+#pragma unroll
+      for (int mb = 0; mb < C::kMB; ++mb) {
+        shift[mb] = 0.f;
+#pragma unroll
+        for (int db = 0; db < C::kDB; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[db][mb][r] = 0.f;
+      }
+      lsum = f32x4{0.f, 0.f, 0.f, 0.f};
+      biased = false;
+      if (n > 0) issue(kreq, kb_addr, 0);
+      if (n > 1) issue(kreq, kb_addr, 1);
+      if (n > 0) issue(vreq, vb_addr, 0);
+      wait_vmem();
+      lds_barrier();
+      run_pass(std::true_type{});
+    }
   }
-  if (active && n > 0) pv_tile(n - 1);
 
   if (active) {
 #pragma unroll
