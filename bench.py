@@ -414,7 +414,7 @@ def main():
                    "step": ("cross_attn + self_attn_step_fused (append + attend)" if fused else
                             "cross_attn + kv_append (copy into slab) + self_attn_step")
                            + ", t = k mod 4"},
-        "roofline": {"bound": "mfma", "kernel": "grace_cross_attn (cross_attn_bf16_dual_kernel<64>)",
+        "roofline": {"bound": "mfma", "kernel": "grace_cross_attn (cross_attn_bf16_kernel<64>)",
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
                      "algorithmic_flops_per_launch": cross_flops,

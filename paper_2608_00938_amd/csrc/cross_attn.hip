@@ -1,20 +1,19 @@
 // Beam-as-query cross-attention for gfx950 (GRACE, Sec. 5.1, App. B).
 //
 // The M beams of request b are the query rows of one contraction against that
-// request's encoder K/V.  A workgroup owns one (request, head, beam tile);
-// K/V stream through LDS in token tiles that every beam of the tile reuses,
-// so each encoder token is read from L2 once per beam tile, not once per beam.
+// request's encoder K/V: O = softmax(scale * Q_b K_b^T) V_b per head.  A
+// workgroup owns one (request, head, beam tile); K/V stream through LDS in
+// token tiles that every beam of the tile reuses, so each encoder token is
+// read from L2 once per beam tile, not once per beam.
 //
-// bf16 path (MFMA, cross_attn_bf16_dual_kernel).  Each wave owns 64 beams
-// (32 at head dim 128) and, per tile, computes
-//   S^T = K Q^T - shift   v_mfma_f32_32x32x16_bf16; A = K rows from LDS, B = Q^T
+// bf16 path (MFMA, cross_attn_bf16_kernel).  Each wave owns 64 beams (32 at
+// head dim 128) and computes, per 32-key step,
+//   S^T = K Q^T           v_mfma_f32_32x32x16_bf16; A = K rows from LDS, B = Q^T
 //                         (pre-multiplied by scale*log2(e)) held in registers,
-//                         plus one rank-1 MFMA that subtracts the beam's shift,
-//                         so S^T holds exp2 arguments directly;
-//   P = exp2(S^T)         VALU, lazily re-shifted when a beam's running max
-//                         grows by more than 8 (exp2 units);
+//                         so S^T holds exp2 arguments;
+//   P = exp2(S^T)         VALU, packed to bf16 in place;
 //   O^T += V^T P^T        A = V^T read with ds_read_b64_tr_b16, B = P^T taken
-//                         straight from the S^T registers as bf16;
+//                         straight from the S^T registers;
 //   l += 1^T P^T          the row sums of the applied bf16 weights, on the
 //                         matrix core as well.
 // The transposed orientation puts one beam per lane column in every product,
@@ -120,11 +119,11 @@ cross_attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k,
 }
 
 // ---------------------------------------------------------------------------
-// bf16 MFMA kernel
+// bf16 MFMA kernel: helpers
 // ---------------------------------------------------------------------------
-// XOR swizzle of the 16-byte chunk index within a token (or beam) row of a
-// tile in LDS: both the 16-row x one-chunk operand reads (K, Q) and the
-// transposed V reads (8 rows x 4 chunks) spread over all bank groups.
+// XOR swizzle of the 16-byte chunk index within a token row of a tile in LDS:
+// both the 16-row x one-chunk operand reads (K) and the transposed V reads
+// (8 rows x 4 chunks) spread over all bank groups.
 template <int D>
 __device__ __forceinline__ int tile_swizzle(int row) {
   if constexpr (D == 32) return (row >> 2) & 3;
@@ -137,7 +136,7 @@ __device__ __forceinline__ int tile_swizzle(int row) {
 // byte address lds_wave_addr + 16 * lane.  base and lds_wave_addr must be
 // wave-uniform (scalar registers).  Issued as inline asm so that the compiler
 // neither waits for it before unrelated LDS reads nor drains it at every
-// barrier: the kernel waits for these loads explicitly (wait_vmem_keep) right
+// barrier: the kernel waits for these loads explicitly (wait_vmem_upto) right
 // before the barrier that publishes the tile they fill.
 __device__ __forceinline__ void load_to_lds(const void* base, uint32_t byte_off,
                                             uint32_t lds_wave_addr) {
@@ -145,17 +144,6 @@ __device__ __forceinline__ void load_to_lds(const void* base, uint32_t byte_off,
                :
                : "v"(byte_off), "s"(base), "s"(lds_wave_addr)
                : "memory", "m0");
-}
-
-// s_waitcnt vmcnt(0) issued as inline asm (the loads above are invisible to
-// the compiler's wait tracking).
-__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
-
-// s_waitcnt vmcnt(n) for the n most recent loads still allowed in flight.
-__device__ __forceinline__ void wait_vmem_keep(int n) {
-  if (n >= 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
-  else if (n >= 2) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
-  else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
 // Workgroup barrier that orders LDS only: pending LDS operations complete,
@@ -195,31 +183,46 @@ __device__ __forceinline__ float max_with_other_half(float x) {
 }
 
 // ---------------------------------------------------------------------------
-// bf16 MFMA kernel, two workgroups per CU (head dims 32, 64 and 128).
+// bf16 MFMA kernel (head dims 32, 64 and 128).
 //
-// A workgroup is four waves (one per SIMD) and two workgroups share each CU,
-// so every SIMD runs two independent waves: while one is in its MFMA phase
-// the other is usually in its softmax phase, and one workgroup's prologue
-// (Q staging) and epilogue (O stores) overlap the other's tiles.
+// Work split.  A workgroup is four waves (one per SIMD) of 32*kMB beams each,
+// and two workgroups share each CU, so every SIMD runs two independent waves.
+// XCD-aware workgroup ordering puts the beam tiles of one (request, head) on
+// one XCD, whose L2 then serves the request's K/V to all of them.
 //
-// Per tile t a wave runs its MFMA phase (O += V(t-1)^T P(t-1)^T and the row
-// sums of P(t-1), then S(t)^T = K(t) Q^T [- shift]) and its softmax phase,
-// then meets the other three waves at one barrier.  K and V each rotate
-// through three LDS buffers: K(t+2) and V(t+1) are issued at the start of
-// tile t and waited for at the end of tile t+1, two tiles after issue; the
-// buffer each load overwrites was last read before the barrier that ended
-// tile t-1.
+// Software pipeline.  Each wave runs over 32-key steps so that its
+// instruction stream always holds independent matrix and vector work:
 //
-// Exponent shift.  exp2 arguments are S^T minus a per-beam shift that starts
-// at 0 and moves only when needed: when the first tile's maximum lies outside
-// [-64, 32] or a later tile's maximum exceeds the shift by more than 32.  Then
-// the shift becomes the running maximum (as a bf16 hi+lo pair, 16 significant
-// bits), O and the row sums are rescaled, and from then on a rank-1 MFMA term
-// subtracts it inside the S^T product.  With the shift bounded this way
-// exp2 never overflows (P <= 2^32) and the largest weight of a beam is at
-// least 2^-64, so the result is the softmax of the definition for any input;
-// with the shift at 0 (scores within those bounds, the common case) the
-// rank-1 term and every rescale are skipped.
+//   step j:  exp2/pack of S(j)^T (VALU)                  -> P(j)
+//            S(j+1)^T = K(j+1) Q^T (MFMA, accumulating)
+//            O^T += V(j)^T P(j)^T and the row sums (MFMA, one chunk behind
+//            the exp2/pack that produces its P; the last chunk is carried
+//            into step j+1)
+//
+// in a fixed issue order: every 32x32x16 product is followed by the VALU work
+// that fits under it (two exp2 at the quarter rate), so that one wave alone
+// keeps both the matrix core and the VALU busy.  Q^T (times scale*log2 e,
+// re-rounded to bf16) stays in registers.
+//
+// Stream.  K and V pass through two four-buffer LDS rings in tiles of kTileN
+// keys, K one tile ahead of V: at the start of tile T the workgroup issues
+// K(T+3) and V(T+2) (direct-to-LDS loads) and at its end waits for K(T+2) and
+// V(T+1) and meets at one barrier, so tile T reads K(T), K(T+1) and V(T) while
+// the buffers being filled were last read before the previous barrier.
+//
+// Softmax.  The fast pass takes no maximum: the scores go straight through
+// exp2.  After the last step each wave checks that every beam's row sum lies
+// in [2^-100, 2^64] and that its O is finite, and the waves vote.  If any beam
+// fails, the whole workgroup redoes its tile with the safe pass (stepwise, not
+// pipelined): an exponent shift per beam that starts at 0 and moves only when
+// the first step's maximum lies outside [-64, 32] or a later step's maximum
+// exceeds the shift by more than 32.  Then the shift becomes the running
+// maximum (a bf16 hi+lo pair, 16 significant bits), O and the row sums are
+// rescaled, and a rank-1 MFMA term subtracts the shift inside the S^T product.
+// With the shift bounded this way exp2 never overflows (P <= 2^32) and the
+// largest weight of a beam is at least 2^-64, so the safe pass gives the
+// softmax of the definition for any input; the fast pass is kept only when its
+// sums prove it neither overflowed nor lost precision to underflow.
 //
 // Row sums.  One v_mfma_f32_16x16x32_bf16 per 16-key chunk and beam block
 // sums the applied bf16 weights: it reads the P^T fragment of the 32x32x16
@@ -228,45 +231,58 @@ __device__ __forceinline__ float max_with_other_half(float x) {
 // the even (odd) groups give the sums of beam c (c+16).
 // ---------------------------------------------------------------------------
 template <int D>
-struct Dual {
+struct Cfg {
   static constexpr int kWaves = 4;
   static constexpr int kThreads = kWaves * 64;
-  static constexpr int kMB = D == 128 ? 1 : 2;        // 32-beam blocks per wave
-  static constexpr int kBlockM = kWaves * kMB * 32;   // beams per workgroup
-  static constexpr int kBlockN = D == 128 ? 32 : 64;  // encoder tokens per tile
-  static constexpr int kKB = kBlockN / 32;
-  static constexpr int kKS = D / 16;
-  static constexpr int kDB = D / 32;
-  static constexpr int kKC = kBlockN / 16;
-  static constexpr int kCPR = D / 8;
-  static constexpr int kSlots = kBlockN * kCPR;
-  static constexpr int kLoads = kSlots / kThreads;    // 16-byte loads per thread per tile and tensor
+  static constexpr int kMB = D == 128 ? 1 : 2;         // 32-beam blocks per wave
+  static constexpr int kBlockM = kWaves * kMB * 32;    // beams per workgroup
+  static constexpr int kTileN = D == 128 ? 32 : 64;    // keys per LDS tile
+  static constexpr int kSub = kTileN / 32;             // 32-key steps per tile
+  static constexpr int kKS = D / 16;                   // 16-wide d steps of QK
+  static constexpr int kDB = D / 32;                   // 32-wide d blocks of O
+  static constexpr int kCPR = D / 8;                   // 16-byte chunks per token row
+  static constexpr int kRowBytes = kCPR * 16;
+  static constexpr int kSlots = kTileN * kCPR;
+  static constexpr int kLoads = kSlots / kThreads;     // loads per thread per tile and tensor
   static constexpr int kTileBytes = kSlots * 16;
-  static constexpr int kNBuf = 3;
-  static constexpr int kQChunks = kBlockM * kCPR / kThreads;
-  static constexpr int kQBytes = kBlockM * D * 2;
-  static constexpr int kLdsBytes = 2 * kNBuf * kTileBytes + kQBytes;
-  static constexpr float kShiftHi = 32.0f;    // re-shift when a tile max exceeds the shift by this
-  static constexpr float kShiftLo = -64.0f;   // ... or the first tile's max is below this
-  static_assert(kSlots % kThreads == 0 && (kBlockM * kCPR) % kThreads == 0, "even split");
-  __device__ __forceinline__ static int swz(int key) { return tile_swizzle<D>(key); }
+  static constexpr int kNBuf = 4;
+  static constexpr int kLdsBytes = 2 * kNBuf * kTileBytes;
+  static constexpr int kUnits = 2 * kMB;               // (16-key chunk, beam block) pairs per step
+  static constexpr int kQKPerUnit = kKS * kMB / kUnits;
+  static constexpr float kShiftHi = 32.0f;
+  static constexpr float kShiftLo = -64.0f;
+  static_assert(kSlots % kThreads == 0 && (kKS * kMB) % kUnits == 0, "even split");
+  static_assert(kLoads * 2 <= 8, "wait_vmem_upto covers up to eight loads per tile");
   __device__ __forceinline__ static int slot(int key, int chunk) {
-    return key * kCPR + (chunk ^ swz(key));
+    return key * kCPR + (chunk ^ tile_swizzle<D>(key));
   }
 };
 
+// s_waitcnt vmcnt(n) for n in [0, 8].
+__device__ __forceinline__ void wait_vmem_upto(int n) {
+  switch (n) {
+    case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    case 1: asm volatile("s_waitcnt vmcnt(1)" ::: "memory"); break;
+    case 2: asm volatile("s_waitcnt vmcnt(2)" ::: "memory"); break;
+    case 3: asm volatile("s_waitcnt vmcnt(3)" ::: "memory"); break;
+    case 4: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
+    case 5: asm volatile("s_waitcnt vmcnt(5)" ::: "memory"); break;
+    case 6: asm volatile("s_waitcnt vmcnt(6)" ::: "memory"); break;
+    case 7: asm volatile("s_waitcnt vmcnt(7)" ::: "memory"); break;
+    default: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+  }
+}
+
 template <int D>
-__global__ void __launch_bounds__(Dual<D>::kThreads, 2)
-cross_attn_bf16_dual_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+__global__ void __launch_bounds__(Cfg<D>::kThreads, 2)
+cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                             const uint16_t* __restrict__ v, const int32_t* __restrict__ off,
                             uint16_t* __restrict__ out, int32_t M, int32_t H, int32_t sum_L,
                             int32_t n_mt, float c) {
-  using C = Dual<D>;
-  static_assert(C::kLoads * 2 <= 4, "wait_vmem_keep covers up to four loads per tile");
+  using C = Cfg<D>;
   __shared__ __attribute__((aligned(16))) char lds[C::kLdsBytes];
-  char* const kbuf0 = lds;                                 // K tiles: 3 buffers
-  char* const vbuf0 = lds + C::kNBuf * C::kTileBytes;      // V tiles: 3 buffers
-  char* const qbuf = lds + 2 * C::kNBuf * C::kTileBytes;   // scaled Q of the beam tile
+  char* const kbuf0 = lds;                              // K ring: 4 tiles
+  char* const vbuf0 = lds + C::kNBuf * C::kTileBytes;   // V ring: 4 tiles
 
   const uint32_t tile = xcd_remap(blockIdx.x, gridDim.x);
   const int32_t mt = tile % n_mt;
@@ -282,6 +298,8 @@ cross_attn_bf16_dual_kernel(const uint16_t* __restrict__ q, const uint16_t* __re
   const int32_t E = H * D;   // 32-bit offsets: B*M*H*d and sum_L*H*d < 2^31 (checked by the API)
   const int32_t m_base = mt * C::kBlockM + wave * (C::kMB * 32);
   const bool active = m_base < M;
+  const int32_t n = (L + C::kTileN - 1) / C::kTileN;   // LDS tiles
+  const int32_t n_sub = (L + 31) / 32;                  // 32-key steps
 
   // Row-sum operands (16x16x32): lane = row (lane & 15), 8-key group lane >> 4.
   bf16x8 sum_a[C::kMB];
@@ -291,31 +309,14 @@ cross_attn_bf16_dual_kernel(const uint16_t* __restrict__ q, const uint16_t* __re
     const uint32_t w = row == 2 * mb + odd ? 0x3f803f80u : 0u;
     sum_a[mb] = __builtin_bit_cast(bf16x8, u32x4{w, w, w, w});
   }
-  float shift[C::kMB];
-  f32x16 o[C::kDB][C::kMB];
-  f32x4 lsum = {0.f, 0.f, 0.f, 0.f};   // lanes 0-15: rows 2mb / 2mb+1 = beams c / c+16 of block mb
-  bool biased = false;                 // some beam of the wave has a non-zero shift
-#pragma unroll
-  for (int mb = 0; mb < C::kMB; ++mb) {
-    shift[mb] = 0.f;
-#pragma unroll
-    for (int db = 0; db < C::kDB; ++db)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[db][mb][r] = 0.f;
-  }
-  f32x16 s[C::kKB][C::kMB];
-  bf16x8 pf[C::kKC][C::kMB];
 
-  const int32_t n = (L + C::kBlockN - 1) / C::kBlockN;
-
-  // This lane's K/V slots of a tile: byte offsets from the tile's first token
-  // row (the same for K and V); the last, partial tile clamps its tokens.
+  // Direct-to-LDS tile loads (one tile of K or V per call).
   uint32_t dma_off[C::kLoads];
 #pragma unroll
   for (int i = 0; i < C::kLoads; ++i) {
     const int sl = i * C::kThreads + threadIdx.x;
     const int key = sl / C::kCPR;
-    const int chunk = (sl % C::kCPR) ^ C::swz(key);
+    const int chunk = (sl % C::kCPR) ^ tile_swizzle<D>(key);
     // modular uint32 arithmetic: offsets of rows past the request may wrap,
     // but every offset actually loaded (after clamping) is below 2^32
     dma_off[i] = ((uint32_t)key * (uint32_t)E + (uint32_t)(h * D + chunk * 8)) * 2u;
@@ -325,10 +326,10 @@ cross_attn_bf16_dual_kernel(const uint16_t* __restrict__ q, const uint16_t* __re
   const uint16_t* const kreq = k + o0 * E;
   const uint16_t* const vreq = v + o0 * E;
   auto issue = [&](const uint16_t* req, uint32_t lds_base, int32_t t) __attribute__((always_inline)) {
-    const int32_t t0 = t * C::kBlockN;
+    const int32_t t0 = t * C::kTileN;
     const uint16_t* base = req + t0 * E;
-    const uint32_t dst = lds_base + (t % C::kNBuf) * C::kTileBytes;
-    if (t0 + C::kBlockN <= L) {
+    const uint32_t dst = lds_base + (t & (C::kNBuf - 1)) * C::kTileBytes;
+    if (t0 + C::kTileN <= L) {
 #pragma unroll
       for (int i = 0; i < C::kLoads; ++i) load_to_lds(base, dma_off[i], dst + i * C::kThreads * 16);
     } else {
@@ -341,14 +342,61 @@ cross_attn_bf16_dual_kernel(const uint16_t* __restrict__ q, const uint16_t* __re
       }
     }
   };
+  // Loads of tile T's start (K(T+3), V(T+2)); returns how many this thread issued.
+  auto prefetch = [&](int32_t T) __attribute__((always_inline)) -> int {
+    int issued = 0;
+    if (T + 3 < n) { issue(kreq, kb_addr, T + 3); issued += C::kLoads; }
+    if (T + 2 < n) { issue(vreq, vb_addr, T + 2); issued += C::kLoads; }
+    return issued;
+  };
+  // Tile T's end: K(T+2) and V(T+1) have landed (the loads of this tile's start
+  // may still fly), then the barrier that publishes them.
+  auto publish = [&](int issued) __attribute__((always_inline)) {
+    wait_vmem_upto(issued);
+    lds_barrier();
+  };
+  // The prologue's loads: K(0), K(1), V(0) now, K(2), V(1) after the queries.
+  auto prologue_early = [&]() __attribute__((always_inline)) {
+    if (n > 0) issue(kreq, kb_addr, 0);
+    if (n > 1) issue(kreq, kb_addr, 1);
+    if (n > 0) issue(vreq, vb_addr, 0);
+  };
+  auto prologue_late = [&]() __attribute__((always_inline)) -> int {
+    int late = 0;
+    if (n > 2) { issue(kreq, kb_addr, 2); late += C::kLoads; }
+    if (n > 1) { issue(vreq, vb_addr, 1); late += C::kLoads; }
+    return late;
+  };
+
+  prologue_early();
+
+  // Q^T fragments (B operand of S^T = K Q^T): lane holds 8 consecutive d of
+  // beam l32 of block mb, for 16-wide d step ks.  Beams past M repeat beam
+  // M-1, whose results are never stored.
+  bf16x8 qf[C::kMB][C::kKS];
+#pragma unroll
+  for (int mb = 0; mb < C::kMB; ++mb) {
+    int32_t m = m_base + mb * 32 + l32;
+    m = m < M ? m : M - 1;
+    const uint16_t* qrow = q + (b * M + m) * E + h * D + 8 * hi;
+#pragma unroll
+    for (int ks = 0; ks < C::kKS; ++ks) {
+      const u32x4 u = *(const u32x4*)(qrow + ks * 16);
+      float f[8];
+      Chunk<BF16>::unpack(u, f);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) f[e] *= c;
+      qf[mb][ks] = __builtin_bit_cast(bf16x8, Chunk<BF16>::pack(f));
+    }
+  }
 
   // LDS read offsets of this lane within a tile.  K (A of S^T): one per
-  // 16-wide d step; the 32-key blocks add kb * 32 rows.  V^T (transposed
-  // reads): one per (8-row half, 32-wide d block); 16-key chunks add kc * 16
-  // rows.  Row strides leave the swizzle unchanged, so they are immediates.
+  // 16-wide d step.  V^T (transposed reads): one per (8-row half, 32-wide d
+  // block).  32-key steps add 32 rows, 16-key chunks 16 rows; row strides keep
+  // the swizzle, so they and the buffer bases are immediates.
   uint32_t k_rd[C::kKS];
 #pragma unroll
-  for (int ks = 0; ks < C::kKS; ++ks) k_rd[ks] = C::slot(l32, 2 * ks + hi) * 16;
+  for (int ks = 0; ks < C::kKS; ++ks) k_rd[ks] = lds_addr(kbuf0) + C::slot(l32, 2 * ks + hi) * 16;
   uint32_t v_rd[2][C::kDB];
   {
     const int g4 = lane >> 4, gi = lane & 15;
@@ -358,335 +406,260 @@ cross_attn_bf16_dual_kernel(const uint16_t* __restrict__ q, const uint16_t* __re
       for (int db = 0; db < C::kDB; ++db) {
         const int dcol = db * 32 + 16 * (g4 & 1) + 4 * (gi & 3);
         const int row = 8 * w + 4 * (g4 >> 1) + (gi >> 2);
-        v_rd[w][db] = C::slot(row, dcol >> 3) * 16 + (dcol & 7) * 2;
+        v_rd[w][db] = lds_addr(vbuf0) + C::slot(row, dcol >> 3) * 16 + (dcol & 7) * 2;
       }
   }
-  constexpr int kKeyRowBytes = C::kCPR * 16;
-
-  // Prologue: the first K/V tiles go out before Q is staged, so their latency
-  // overlaps the Q loads; one wait covers both.
-  if (n > 0) issue(kreq, kb_addr, 0);
-  if (n > 1) issue(kreq, kb_addr, 1);
-  if (n > 0) issue(vreq, vb_addr, 0);
-  // Stage Q (times c = scale*log2(e), re-rounded to bf16) in the K-tile slot
-  // layout; beams past M repeat beam M-1, whose results are never stored.
-#pragma unroll
-  for (int i = 0; i < C::kQChunks; ++i) {
-    const int sl = i * C::kThreads + threadIdx.x;
-    const int beam = sl / C::kCPR;
-    const int chunk = (sl % C::kCPR) ^ C::swz(beam);
-    int32_t m = mt * C::kBlockM + beam;
-    m = m < M ? m : M - 1;
-    const u32x4 u = *(const u32x4*)(q + (b * M + m) * E + h * D + chunk * 8);
-    float f[8];
-    Chunk<BF16>::unpack(u, f);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) f[e] *= c;
-    *(u32x4*)(qbuf + sl * 16) = Chunk<BF16>::pack(f);
-  }
-
-  wait_vmem();                          // K(0), K(1), V(0) have landed
-  lds_barrier();
-
-  // Q^T fragments of this wave's beams.  At head dim 32 they stay in
-  // registers for all tiles; at 64 and 128 they are re-read from LDS with the
-  // K fragments of every tile (Q sits in the same slot layout, so the K read
-  // offsets serve), which keeps the exp/PV phase within the register budget.
-  constexpr bool kQInRegs = D == 32;
-  const char* const qwave = qbuf + wave * (C::kMB * 32) * C::kCPR * 16;
-  bf16x8 qf_res[kQInRegs ? C::kMB : 1][kQInRegs ? C::kKS : 1];
-  if constexpr (kQInRegs) {
-#pragma unroll
-    for (int mb = 0; mb < C::kMB; ++mb)
-#pragma unroll
-      for (int ks = 0; ks < C::kKS; ++ks)
-        qf_res[mb][ks] = __builtin_bit_cast(
-            bf16x8, *(const u32x4*)(qwave + k_rd[ks] + mb * 32 * C::kCPR * 16));
-  }
-
-  // S(t)^T = K(t) Q^T, starting from the shift term or from zero.
-  auto qk = [&](const char* kbp, auto with_shift) __attribute__((always_inline)) {
-    // K and Q fragments of one 16-wide d step, loaded one step ahead.
-    auto load_ks = [&](int ks, bf16x8 (&kf)[C::kKB], bf16x8 (&qf)[C::kMB])
-        __attribute__((always_inline)) {
-#pragma unroll
-      for (int kb = 0; kb < C::kKB; ++kb)
-        kf[kb] = __builtin_bit_cast(bf16x8,
-                                    *(const u32x4*)(kbp + k_rd[ks] + kb * 32 * kKeyRowBytes));
-#pragma unroll
-      for (int mb = 0; mb < C::kMB; ++mb) {
-        if constexpr (kQInRegs)
-          qf[mb] = qf_res[mb][ks];
-        else
-          qf[mb] = __builtin_bit_cast(
-              bf16x8, *(const u32x4*)(qwave + k_rd[ks] + mb * 32 * kKeyRowBytes));
-      }
-    };
-    bf16x8 kf[2][C::kKB], qf[2][C::kMB];
-    load_ks(0, kf[0], qf[0]);
-    const f32x16 zero = {};
-#pragma unroll
-    for (int ks = 0; ks < C::kKS; ++ks) {
-      if (ks + 1 < C::kKS) load_ks(ks + 1, kf[(ks + 1) & 1], qf[(ks + 1) & 1]);
-      const bf16x8(&k)[C::kKB] = kf[ks & 1];
-      const bf16x8(&qq)[C::kMB] = qf[ks & 1];
-#pragma unroll
-      for (int kb = 0; kb < C::kKB; ++kb)
-#pragma unroll
-        for (int mb = 0; mb < C::kMB; ++mb) {
-          if (ks > 0) {
-            s[kb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k[kb], qq[mb], s[kb][mb], 0, 0, 0);
-          } else if constexpr (decltype(with_shift)::value) {
-            // Rank-1 term S^T += 1 * (-shift): A has 1 in k-slots 0 and 1 of
-            // lanes 0-31, B carries -shift of the lane's beam as a bf16 pair
-            // (hi, lo) in those slots, so the MFMA adds exactly the 16-bit
-            // shift (shift is a sum of two bf16 values).
-            const float nhi = round_to_bf16(-shift[mb]);
-            const uint32_t nb = pack_bf16x2(nhi, -shift[mb] - nhi);
-            const bf16x8 one_a =
-                __builtin_bit_cast(bf16x8, u32x4{hi == 0 ? 0x3f803f80u : 0u, 0u, 0u, 0u});
-            const bf16x8 bias_b =
-                __builtin_bit_cast(bf16x8, u32x4{hi == 0 ? nb : 0u, 0u, 0u, 0u});
-            s[kb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                k[kb], qq[mb],
-                __builtin_amdgcn_mfma_f32_32x32x16_bf16(one_a, bias_b, zero, 0, 0, 0), 0, 0, 0);
-          } else {
-            s[kb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k[kb], qq[mb], zero, 0, 0, 0);
-          }
-        }
-    }
+  typedef __attribute__((address_space(3))) char lds_char;
+  // K fragment of d step ks for the 32-key step `sub` of the tile in buffer `buf`.
+  auto read_k = [&](int buf, int sub, int ks) __attribute__((always_inline)) -> bf16x8 {
+    return __builtin_bit_cast(
+        bf16x8, *(const __attribute__((address_space(3))) u32x4*)(
+                    (lds_char*)(uintptr_t)k_rd[ks] + buf * C::kTileBytes + sub * 32 * C::kRowBytes));
   };
-
-  // V(t)^T fragments (transposed LDS reads) of 16-key chunk kc.
-  auto read_v = [&](int32_t t, int kc, bf16x8 (&vf)[C::kDB]) __attribute__((always_inline)) {
-    const char* vb = vbuf0 + (t % C::kNBuf) * C::kTileBytes;
+  // V^T fragments of 16-key chunk kc of the 32-key step `sub` of buffer `buf`.
+  auto read_v = [&](int buf, int sub, int kc, bf16x8 (&vf)[C::kDB]) __attribute__((always_inline)) {
 #pragma unroll
     for (int db = 0; db < C::kDB; ++db) {
       i16x4 part[2];
 #pragma unroll
       for (int w = 0; w < 2; ++w)
         part[w] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) i16x4*)(
-                (__attribute__((address_space(3))) char*)vb + v_rd[w][db] +
-                kc * 16 * kKeyRowBytes));
+            (__attribute__((address_space(3))) i16x4*)((lds_char*)(uintptr_t)v_rd[w][db] +
+                                                         buf * C::kTileBytes +
+                                                         (2 * sub + kc) * 16 * C::kRowBytes));
       typedef short i16x8 __attribute__((ext_vector_type(8)));
       const i16x8 both = __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7);
       vf[db] = __builtin_bit_cast(bf16x8, both);
     }
   };
-  // O += V^T P^T and the row sums of P for chunk kc, beam block mb.
-  auto pv_chunk = [&](const bf16x8 (&vf)[C::kDB], int kc, int mb) __attribute__((always_inline)) {
-#pragma unroll
-    for (int db = 0; db < C::kDB; ++db)
-      o[db][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db], pf[kc][mb], o[db][mb], 0, 0, 0);
-    lsum = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sum_a[mb], pf[kc][mb], lsum, 0, 0, 0);
-  };
-  // P = exp2(S^T) for chunk kc, beam block mb, as a bf16 fragment over pf.
-  auto exp_chunk = [&](int kc, int mb) __attribute__((always_inline)) {
-    const int kb = kc >> 1, r0 = 8 * (kc & 1);
-#pragma unroll
-    for (int r = 0; r < 8; ++r) s[kb][mb][r0 + r] = fast_exp2(s[kb][mb][r0 + r]);
-    const u32x4 u = {pack_bf16x2(s[kb][mb][r0 + 0], s[kb][mb][r0 + 1]),
-                     pack_bf16x2(s[kb][mb][r0 + 2], s[kb][mb][r0 + 3]),
-                     pack_bf16x2(s[kb][mb][r0 + 4], s[kb][mb][r0 + 5]),
-                     pack_bf16x2(s[kb][mb][r0 + 6], s[kb][mb][r0 + 7])};
-    pf[kc][mb] = __builtin_bit_cast(bf16x8, u);
-  };
-  // All of tile t's P into O (V chunks read one ahead of their MFMAs).
-  auto pv_tile = [&](int32_t t) __attribute__((always_inline)) {
-    bf16x8 vf[2][C::kDB];
-    read_v(t, 0, vf[0]);
-#pragma unroll
-    for (int kc = 0; kc < C::kKC; ++kc) {
-      if (kc + 1 < C::kKC) read_v(t, kc + 1, vf[(kc + 1) & 1]);
-#pragma unroll
-      for (int mb = 0; mb < C::kMB; ++mb) pv_chunk(vf[kc & 1], kc, mb);
-    }
-  };
-  // pv_tile(t - 1) fused with the exp/pack of tile t: chunk by chunk, the
-  // MFMAs read P(t-1) from pf, then exp/pack writes P(t) into the same
-  // registers; the scheduler interleaves each chunk's MFMAs with its VALU work.
-  constexpr int kChunkMfma = C::kDB + 1;   // per (chunk, beam block)
-  constexpr int kChunkValu = 8 + 4;        // 8 exp2 + 4 packs
-  auto pv_exp_tile = [&](int32_t tv) __attribute__((always_inline)) {
-    bf16x8 vf[2][C::kDB];
-    read_v(tv, 0, vf[0]);
-#pragma unroll
-    for (int kc = 0; kc < C::kKC; ++kc) {
-      if (kc + 1 < C::kKC) read_v(tv, kc + 1, vf[(kc + 1) & 1]);
-#pragma unroll
-      for (int mb = 0; mb < C::kMB; ++mb) {
-        pv_chunk(vf[kc & 1], kc, mb);
-        exp_chunk(kc, mb);
-      }
-    }
-    // Pin P(t) here: without a use in this block the compiler sinks the
-    // exp/pack work below the (rare) rescale branch, away from the MFMAs.
-#pragma unroll
-    for (int kc = 0; kc < C::kKC; ++kc)
-#pragma unroll
-      for (int mb = 0; mb < C::kMB; ++mb) asm volatile("" ::"v"(pf[kc][mb]));
-    constexpr int kV = kChunkValu / kChunkMfma;
-    constexpr int kVLast = kChunkValu - (kChunkMfma - 1) * kV;
-#pragma unroll
-    for (int g = 0; g < C::kKC * C::kMB; ++g) {
-#pragma unroll
-      for (int i = 0; i + 1 < kChunkMfma; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // one MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, kV, 0);   // then VALU
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, kVLast, 0);
-    }
-  };
 
-  // Softmax bookkeeping of tile t on S(t)^T: mask the keys past L, take each
-  // beam's maximum and, when a beam needs it (rare), move its shift.
-  // Keys past L in the last, partial tile get weight 0.
-  auto mask_tail = [&](int32_t t) __attribute__((always_inline)) {
-    const int32_t t0 = t * C::kBlockN;
-    if (t0 + C::kBlockN > L) {
-#pragma unroll
-      for (int kb = 0; kb < C::kKB; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = t0 + kb * 32 + 8 * (r >> 2) + 4 * hi + (r & 3);
-          if (key >= L) {
-#pragma unroll
-            for (int mb = 0; mb < C::kMB; ++mb) s[kb][mb][r] = -INFINITY;
-          }
-        }
-    }
-  };
-  float alpha[C::kMB];
-  auto softmax_shift = [&](int32_t t) __attribute__((always_inline)) -> bool {
-    mask_tail(t);
-    float mx[C::kMB];
-    bool any = false;
+  f32x16 o[C::kDB][C::kMB];
+  f32x4 lsum = {0.f, 0.f, 0.f, 0.f};   // lanes 0-15: rows 2mb / 2mb+1 = beams c / c+16 of block mb
+  float shift[C::kMB];
+  bool biased = false;
+  auto reset_acc = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int mb = 0; mb < C::kMB; ++mb) {
-      // two independent max3 chains over the 16*kKB scores of the lane
-      float m0 = max3(s[0][mb][0], s[0][mb][1], s[0][mb][2]);
-      float m1 = max3(s[0][mb][3], s[0][mb][4], s[0][mb][5]);
-#pragma unroll
-      for (int i = 6; i + 3 < 16 * C::kKB; i += 4) {
-        m0 = max3(m0, s[i >> 4][mb][i & 15], s[(i + 1) >> 4][mb][(i + 1) & 15]);
-        m1 = max3(m1, s[(i + 2) >> 4][mb][(i + 2) & 15], s[(i + 3) >> 4][mb][(i + 3) & 15]);
-      }
-      // 16*kKB = 6 + 4j + 2: two scores left
-      const float m = max3(max3(m0, m1, s[C::kKB - 1][mb][14]), s[C::kKB - 1][mb][15],
-                           s[C::kKB - 1][mb][15]);
-      mx[mb] = max_with_other_half(m);
-      any |= t == 0 ? (mx[mb] > C::kShiftHi || mx[mb] < C::kShiftLo) : mx[mb] > C::kShiftHi;
-    }
-    if (__builtin_expect(__any(any), 0)) {
-      // Move the shift of the beams that need it to their maximum.  O and the
-      // row sums still lack P(t-1), which was weighted with the old shift:
-      // they are rescaled by alpha once it is in (rescale_after).
-#pragma unroll
-      for (int mb = 0; mb < C::kMB; ++mb) {
-        const bool need =
-            t == 0 ? (mx[mb] > C::kShiftHi || mx[mb] < C::kShiftLo) : mx[mb] > C::kShiftHi;
-        const float ns = need ? round_to_bf16x2(shift[mb] + mx[mb]) : shift[mb];
-        const float delta = ns - shift[mb];
-        alpha[mb] = fast_exp2(-delta);
-        shift[mb] = ns;
-#pragma unroll
-        for (int kb = 0; kb < C::kKB; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) s[kb][mb][r] -= delta;
-      }
-      biased = true;
-      return true;
-    }
-    return false;
-  };
-  // O *= alpha and row sums *= alpha, per beam.
-  auto rescale_after = [&]() __attribute__((always_inline)) {
-#pragma unroll
-    for (int mb = 0; mb < C::kMB; ++mb) {
-      // row sums: lanes 0-15 hold beam c (row 2mb) and beam c+16 (row 2mb+1)
-      const float alpha_hi = __shfl_xor(alpha[mb], 16);
-      lsum[2 * mb] *= alpha[mb];
-      lsum[2 * mb + 1] *= alpha_hi;
+      shift[mb] = 0.f;
 #pragma unroll
       for (int db = 0; db < C::kDB; ++db)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[db][mb][r] *= alpha[mb];
+        for (int r = 0; r < 16; ++r) o[db][mb][r] = 0.f;
+    }
+    lsum = f32x4{0.f, 0.f, 0.f, 0.f};
+    biased = false;
+  };
+  reset_acc();
+
+  // O += V^T P^T and the row sums of P, one 16-key chunk of beam block mb.
+  auto pv = [&](const bf16x8 (&vf)[C::kDB], const bf16x8& p, int mb) __attribute__((always_inline)) {
+#pragma unroll
+    for (int db = 0; db < C::kDB; ++db)
+      o[db][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db], p, o[db][mb], 0, 0, 0);
+    lsum = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sum_a[mb], p, lsum, 0, 0, 0);
+  };
+  // exp2 of rows 8kc..8kc+7 of S^T block mb, packed to bf16 (a P^T fragment).
+  auto exp_pack = [&](f32x16& s, int kc) __attribute__((always_inline)) -> bf16x8 {
+    const int r0 = 8 * kc;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) s[r0 + r] = fast_exp2(s[r0 + r]);
+    const u32x4 u = {pack_bf16x2(s[r0 + 0], s[r0 + 1]), pack_bf16x2(s[r0 + 2], s[r0 + 3]),
+                     pack_bf16x2(s[r0 + 4], s[r0 + 5]), pack_bf16x2(s[r0 + 6], s[r0 + 7])};
+    return __builtin_bit_cast(bf16x8, u);
+  };
+  // Keys at or past L in step j get weight 0.
+  auto mask_step = [&](f32x16 (&s)[C::kMB], int32_t j) __attribute__((always_inline)) {
+    const int32_t k0 = j * 32;
+    if (k0 + 32 > L) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = k0 + 8 * (r >> 2) + 4 * hi + (r & 3);
+        if (key >= L) {
+#pragma unroll
+          for (int mb = 0; mb < C::kMB; ++mb) s[mb][r] = -INFINITY;
+        }
+      }
     }
   };
-  // Loads for tiles ahead of t, then (after this tile's work) the wait for
-  // K(t+1) and V(t) and the barrier that publishes them.
-  auto prefetch = [&](int32_t t) __attribute__((always_inline)) -> int {
-    int issued = 0;
-    if (t + 2 < n) { issue(kreq, kb_addr, t + 2); issued += C::kLoads; }
-    if (t + 1 < n) { issue(vreq, vb_addr, t + 1); issued += C::kLoads; }
-    return issued;
-  };
-  auto publish = [&](int issued) __attribute__((always_inline)) {
-    wait_vmem_keep(issued);   // K(t+1) and V(t) have landed; K(t+2), V(t+1) may fly
+  const f32x16 zero16 = {};
+
+  // ------------------------------ fast pass ------------------------------
+  {
+    // Two register sets, alternated by the parity of the step index (the tile
+    // loop is unrolled over the ring, so parities are known at compile time):
+    // scores of the current and the next step, and V^T fragments of a step's
+    // two 16-key chunks, the second of which serves the chunk carried into the
+    // next step.
+    f32x16 s_set[2][C::kMB];
+    bf16x8 v_set[2][2][C::kDB];
+    bf16x8 pf[2][C::kMB];
+    // The first step's carried chunk is an exact zero product.
+#pragma unroll
+    for (int db = 0; db < C::kDB; ++db)
+      v_set[1][1][db] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+#pragma unroll
+    for (int mb = 0; mb < C::kMB; ++mb)
+      pf[1][mb] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+
+    const int late = prologue_late();
+    wait_vmem_upto(late);   // K(0), K(1), V(0) have landed
     lds_barrier();
-  };
 
-  // One pass over the request's tokens.  Tile t: S(t)^T on the matrix core;
-  // then the softmax of tile t on the VALU with the MFMAs of
-  // O += V(t-1)^T P(t-1)^T interleaved into its exp/pack stream, so one wave
-  // keeps both pipes busy.  Tile 0 has no P before it and the last P is
-  // accumulated after the loop.
-  //   fast pass (SAFE = false): the exponent shift stays 0 and no maximum is
-  //     taken; the result is kept only if every beam's row sum lands in
-  //     [2^-100, 2^64] and its outputs are finite (no overflow, no lost
-  //     precision to underflow);
-  //   safe pass (SAFE = true): the bookkeeping of the exponent shift described
-  //     above, valid for any input.  Run by the whole workgroup when any of its
-  //     beams failed the fast pass's check.
-  auto run_pass = [&](auto safe) __attribute__((always_inline)) {
-    constexpr bool SAFE = decltype(safe)::value;
-    auto s_tile = [&](int32_t t) __attribute__((always_inline)) {
-      const char* kbp = kbuf0 + (t % C::kNBuf) * C::kTileBytes;
-      if (SAFE && biased)
-        qk(kbp, std::true_type{});
-      else
-        qk(kbp, std::false_type{});
+
+    // Step j (parity P): K of step j+1 from buffer kbuf (32-key step ksub of
+    // that tile), V of step j from buffer vbuf (step vsub).  The scores of
+    // step j+1 past the last step are computed from stale LDS and never used.
+    //
+    // Unit u = (16-key chunk kc, beam block mb) issues, in this order: its QK
+    // products, the PV products and row sum of the previous unit (unit 0: the
+    // chunk carried from step j-1), each followed by a slice of its own VALU
+    // work (8 exp2, then 4 packs), so that one wave keeps both the matrix
+    // core and the VALU busy; fences keep the compiler from regrouping them.
+    // LDS fragments are read one unit ahead of their products; with two steps
+    // per tile, the first K fragments of step j+1 are read during step j (the
+    // tile they come from was published one tile early).
+    constexpr bool kCrossPrefetch = C::kSub == 2;
+    bf16x8 kf_next[C::kQKPerUnit];   // first unit's K fragments of the next step
+    auto unit_ks = [](int u, int qq) { return (u * C::kQKPerUnit + qq) / C::kMB; };
+    auto read_unit_k = [&](int kbuf, int ksub, int u, bf16x8 (&kf)[C::kQKPerUnit])
+                           __attribute__((always_inline)) {
+#pragma unroll
+      for (int qq = 0; qq < C::kQKPerUnit; ++qq)
+        if (qq == 0 || unit_ks(u, qq) != unit_ks(u, qq - 1)) kf[qq] = read_k(kbuf, ksub, unit_ks(u, qq));
+#pragma unroll
+      for (int qq = 1; qq < C::kQKPerUnit; ++qq)
+        if (unit_ks(u, qq) == unit_ks(u, qq - 1)) kf[qq] = kf[qq - 1];
     };
-    if (n > 0) {
-      const int issued = prefetch(0);
-      if (active) {
-        s_tile(0);
-        if constexpr (SAFE)
-          softmax_shift(0);   // O and the row sums are still zero: no rescale
-        else
-          mask_tail(0);
+    auto step = [&](int32_t j, auto parity, int kbuf, int ksub, int vbuf, int vsub,
+                    int kbuf_n, int ksub_n) __attribute__((always_inline)) {
+      constexpr int P = decltype(parity)::value;
+      f32x16(&s_cur)[C::kMB] = s_set[P];
+      f32x16(&s_nxt)[C::kMB] = s_set[P ^ 1];
+      bf16x8(&vf)[2][C::kDB] = v_set[P];
+      const bf16x8(&vf_carry)[C::kDB] = v_set[P ^ 1][1];
+      mask_step(s_cur, j);
+      bf16x8 kf[2][C::kQKPerUnit];
+      if constexpr (kCrossPrefetch) {
 #pragma unroll
-        for (int kc = 0; kc < C::kKC; ++kc)
+        for (int qq = 0; qq < C::kQKPerUnit; ++qq) kf[0][qq] = kf_next[qq];
+      } else {
+        read_unit_k(kbuf, ksub, 0, kf[0]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-          for (int mb = 0; mb < C::kMB; ++mb) exp_chunk(kc, mb);
+      for (int u = 0; u < C::kUnits; ++u) {
+        const int kc = u / C::kMB, mb = u % C::kMB;
+        // LDS reads for what comes next
+        if (u == 0) read_v(vbuf, vsub, 0, vf[0]);
+        if (u == (C::kMB > 1 ? C::kMB - 1 : 0)) read_v(vbuf, vsub, 1, vf[1]);
+        if (u + 1 < C::kUnits)
+          read_unit_k(kbuf, ksub, u + 1, kf[(u + 1) & 1]);
+        else if constexpr (kCrossPrefetch)
+          read_unit_k(kbuf_n, ksub_n, 0, kf_next);
+        __builtin_amdgcn_sched_barrier(0);
+        // this unit's VALU work, handed out in slices after each product
+        f32x16& s = s_cur[mb];
+        const int r0 = 8 * kc;
+        u32x4 pw;
+        int next_item = 0;
+        constexpr int kM = C::kQKPerUnit + C::kDB;
+        constexpr int kSlice = 8 / kM > 0 ? 8 / kM : 1;
+        auto valu = [&](int count) __attribute__((always_inline)) {
+#pragma unroll
+          for (int c2 = 0; c2 < count; ++c2) {
+            const int it = next_item + c2;
+            if (it < 8) {
+              s[r0 + it] = fast_exp2(s[r0 + it]);
+            } else if (it < 12) {
+              const int w = it - 8;
+              pw[w] = pack_bf16x2(s[r0 + 2 * w], s[r0 + 2 * w + 1]);
+            }
+          }
+          next_item += count;
+        };
+        // QK products of S(j+1)^T
+#pragma unroll
+        for (int qq = 0; qq < C::kQKPerUnit; ++qq) {
+          const int qi = u * C::kQKPerUnit + qq;
+          const int ks = qi / C::kMB, mq = qi % C::kMB;
+          s_nxt[mq] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[u & 1][qq], qf[mq][ks],
+                                                              ks == 0 ? zero16 : s_nxt[mq], 0, 0, 0);
+          valu(kSlice);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        // PV of the previous chunk
+        const bf16x8(&pvv)[C::kDB] = u == 0 ? vf_carry : vf[(u - 1) / C::kMB];
+        const int pc = u == 0 ? 1 : (u - 1) / C::kMB;
+        const int pm = u == 0 ? C::kMB - 1 : (u - 1) % C::kMB;
+#pragma unroll
+        for (int db = 0; db < C::kDB; ++db) {
+          o[db][pm] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pvv[db], pf[pc][pm], o[db][pm], 0, 0, 0);
+          valu(kSlice);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        lsum = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sum_a[pm], pf[pc][pm], lsum, 0, 0, 0);
+        valu(12 - next_item);
+        pf[kc][mb] = __builtin_bit_cast(bf16x8, pw);
+        __builtin_amdgcn_sched_barrier(0);
       }
-      publish(issued);
-    }
-    for (int32_t t = 1; t < n; ++t) {
-      const int issued = prefetch(t);
-      if (active) {
-        s_tile(t);
-        bool moved = false;
-        if constexpr (SAFE)
-          moved = softmax_shift(t);
-        else
-          mask_tail(t);
-        pv_exp_tile(t - 1);
-        if (SAFE && __builtin_expect(moved, 0)) rescale_after();
-      }
-      publish(issued);
-    }
-    if (active && n > 0) pv_tile(n - 1);
-  };
+    };
 
-  run_pass(std::false_type{});
+    // S(0)^T, and the first K fragments of step 0 (they belong to step 1)
+    if (active && n_sub > 0) {
+#pragma unroll
+      for (int ks = 0; ks < C::kKS; ++ks) {
+        const bf16x8 kf = read_k(0, 0, ks);
+#pragma unroll
+        for (int mb = 0; mb < C::kMB; ++mb)
+          s_set[0][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              kf, qf[mb][ks], ks == 0 ? zero16 : s_set[0][mb], 0, 0, 0);
+      }
+      if constexpr (kCrossPrefetch) read_unit_k(0, 1, 0, kf_next);
+    }
+
+    for (int32_t T0 = 0; T0 < n; T0 += C::kNBuf) {
+#pragma unroll
+      for (int i = 0; i < C::kNBuf; ++i) {
+        const int32_t T = T0 + i;
+        if (T < n) {
+          const int issued = prefetch(T);
+          if (active) {
+#pragma unroll
+            for (int s = 0; s < C::kSub; ++s) {
+              const int32_t j = T * C::kSub + s;
+              if (j < n_sub) {
+                // K of step j+1 (this step's QK) and of step j+2 (prefetched)
+                const int kb = s + 1 < C::kSub ? i : (i + 1) & (C::kNBuf - 1);
+                const int kb2 = s + 2 < C::kSub ? i : (s + 2 < 2 * C::kSub ? (i + 1) & (C::kNBuf - 1)
+                                                                           : (i + 2) & (C::kNBuf - 1));
+                // T0 * kSub is even, so step j's parity is that of i * kSub + s
+                if (((i * C::kSub + s) & 1) == 0)
+                  step(j, std::integral_constant<int, 0>{}, kb, (s + 1) % C::kSub, i, s, kb2,
+                       (s + 2) % C::kSub);
+                else
+                  step(j, std::integral_constant<int, 1>{}, kb, (s + 1) % C::kSub, i, s, kb2,
+                       (s + 2) % C::kSub);
+              }
+            }
+          }
+          publish(issued);
+        }
+      }
+    }
+    // the last step's carried chunk
+    if (active && n_sub > 0) {
+      if ((n_sub - 1) & 1)
+        pv(v_set[1][1], pf[1][C::kMB - 1], C::kMB - 1);
+      else
+        pv(v_set[0][1], pf[1][C::kMB - 1], C::kMB - 1);
+    }
+  }
 
   // Keep the fast pass only if every beam of the workgroup passes the check.
+  bool rerun = false;
   {
     bool bad = false;
-    if (active && n > 0) {
+    if (active && n_sub > 0) {
 #pragma unroll
       for (int mb = 0; mb < C::kMB; ++mb) {
         const float l = lsum[2 * mb], l2 = lsum[2 * mb + 1];   // lanes 0-15 hold the sums
@@ -700,35 +673,99 @@ cross_attn_bf16_dual_kernel(const uint16_t* __restrict__ q, const uint16_t* __re
         bad |= chk != 0.f;   // inf * 0 and NaN * 0 are NaN
       }
     }
-    // One vote word per wave in K buffer 2: no wave reads K after the last
-    // tile's barrier, and the buffer is next written after the rerun's
-    // prologue barrier (K(2)), by which time every wave has read the votes.
-    // (An extra __shared__ word would push two workgroups past the CU's LDS.)
-    int32_t* votes = (int32_t*)(kbuf0 + 2 * C::kTileBytes);
+    // One vote word per wave in K buffer 3: every load has landed and no wave
+    // reads LDS after the last tile's barrier, and the rerun's prologue fills
+    // K buffers 0-2 and V buffers 0-1 only; K buffer 3 is next written at the
+    // rerun's first tile, after its prologue barrier.
+    int32_t* votes = (int32_t*)(kbuf0 + 3 * C::kTileBytes);
     const bool wave_bad = __any(bad);
     if (lane == 0) votes[wave] = wave_bad ? 1 : 0;
     lds_barrier();
-    bool rerun = false;
 #pragma unroll
     for (int w = 0; w < C::kWaves; ++w) rerun |= votes[w] != 0;
-    if (rerun) {
-      // rare: the whole workgroup redoes the tokens with the exponent shift
+  }
+
+  // ------------------------------ safe pass ------------------------------
+  if (rerun) {
+    reset_acc();
+    prologue_early();
+    const int late = prologue_late();
+    wait_vmem_upto(late);
+    lds_barrier();
+    float alpha[C::kMB];
+    for (int32_t T = 0; T < n; ++T) {
+      const int issued = prefetch(T);
+      const int buf = T & (C::kNBuf - 1);
+      if (active) {
+        for (int s = 0; s < C::kSub; ++s) {
+          const int32_t j = T * C::kSub + s;
+          if (j >= n_sub) break;
+          // S(j)^T, minus the shift as a rank-1 term when any beam has one
+          f32x16 sc[C::kMB];
 #pragma unroll
-      for (int mb = 0; mb < C::kMB; ++mb) {
-        shift[mb] = 0.f;
+          for (int mb = 0; mb < C::kMB; ++mb) {
+            sc[mb] = zero16;
+            if (biased) {
+              const float nhi = round_to_bf16(-shift[mb]);
+              const uint32_t nb = pack_bf16x2(nhi, -shift[mb] - nhi);
+              const bf16x8 one_a =
+                  __builtin_bit_cast(bf16x8, u32x4{hi == 0 ? 0x3f803f80u : 0u, 0u, 0u, 0u});
+              const bf16x8 bias_b = __builtin_bit_cast(bf16x8, u32x4{hi == 0 ? nb : 0u, 0u, 0u, 0u});
+              sc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(one_a, bias_b, zero16, 0, 0, 0);
+            }
+          }
 #pragma unroll
-        for (int db = 0; db < C::kDB; ++db)
+          for (int ks = 0; ks < C::kKS; ++ks) {
+            const bf16x8 kf = read_k(buf, s, ks);
 #pragma unroll
-          for (int r = 0; r < 16; ++r) o[db][mb][r] = 0.f;
+            for (int mb = 0; mb < C::kMB; ++mb)
+              sc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[mb][ks], sc[mb], 0, 0, 0);
+          }
+          mask_step(sc, j);
+          // each beam's maximum; move the shift of beams that need it
+          float mx[C::kMB];
+          bool any = false;
+#pragma unroll
+          for (int mb = 0; mb < C::kMB; ++mb) {
+            float m0 = max3(sc[mb][0], sc[mb][1], sc[mb][2]);
+#pragma unroll
+            for (int r = 3; r + 1 < 16; r += 2) m0 = max3(m0, sc[mb][r], sc[mb][r + 1]);
+            m0 = max3(m0, sc[mb][15], sc[mb][15]);
+            mx[mb] = max_with_other_half(m0);
+            any |= j == 0 ? (mx[mb] > C::kShiftHi || mx[mb] < C::kShiftLo) : mx[mb] > C::kShiftHi;
+          }
+          if (__any(any)) {
+#pragma unroll
+            for (int mb = 0; mb < C::kMB; ++mb) {
+              const bool need =
+                  j == 0 ? (mx[mb] > C::kShiftHi || mx[mb] < C::kShiftLo) : mx[mb] > C::kShiftHi;
+              const float ns = need ? round_to_bf16x2(shift[mb] + mx[mb]) : shift[mb];
+              const float delta = ns - shift[mb];
+              alpha[mb] = fast_exp2(-delta);
+              shift[mb] = ns;
+#pragma unroll
+              for (int r = 0; r < 16; ++r) sc[mb][r] -= delta;
+              // O and the row sums hold only weights of the old shift
+              const float alpha_hi = __shfl_xor(alpha[mb], 16);
+              lsum[2 * mb] *= alpha[mb];
+              lsum[2 * mb + 1] *= alpha_hi;
+#pragma unroll
+              for (int db = 0; db < C::kDB; ++db)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) o[db][mb][r] *= alpha[mb];
+            }
+            biased = true;
+          }
+#pragma unroll
+          for (int kc = 0; kc < 2; ++kc) {
+            bf16x8 vfs[C::kDB];
+            read_v(buf, s, kc, vfs);
+#pragma unroll
+            for (int mb = 0; mb < C::kMB; ++mb) pv(vfs, exp_pack(sc[mb], kc), mb);
+          }
+        }
       }
-      lsum = f32x4{0.f, 0.f, 0.f, 0.f};
-      biased = false;
-      if (n > 0) issue(kreq, kb_addr, 0);
-      if (n > 1) issue(kreq, kb_addr, 1);
-      if (n > 0) issue(vreq, vb_addr, 0);
-      wait_vmem();
-      lds_barrier();
-      run_pass(std::true_type{});
+      publish(issued);
     }
   }
 
@@ -764,10 +801,10 @@ hipError_t launch_cross_attn(const void* q, const void* enc_k, const void* enc_v
   if (bf16) {
 #define GRACE_X(DD)                                                                           \
   {                                                                                           \
-    const int32_t n_mt = (M + Dual<DD>::kBlockM - 1) / Dual<DD>::kBlockM;                    \
+    const int32_t n_mt = (M + Cfg<DD>::kBlockM - 1) / Cfg<DD>::kBlockM;                    \
     const int64_t grid = (int64_t)B * H * n_mt;                                              \
-    hipLaunchKernelGGL(cross_attn_bf16_dual_kernel<DD>, dim3((unsigned)grid),                 \
-                       dim3(Dual<DD>::kThreads), 0, stream, (const uint16_t*)q,               \
+    hipLaunchKernelGGL(cross_attn_bf16_kernel<DD>, dim3((unsigned)grid),                 \
+                       dim3(Cfg<DD>::kThreads), 0, stream, (const uint16_t*)q,               \
                        (const uint16_t*)enc_k, (const uint16_t*)enc_v, enc_off, (uint16_t*)out, \
                        M, H, sum_L, n_mt, c);                                                 \
     return hipGetLastError();                                                                 \
