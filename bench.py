@@ -244,6 +244,56 @@ def bench_decode_loop(dev, name="bf16_b8_m256", layers=3, reps=20):
             "graph_us": round(graph, 1), "note": "side measurement, not part of value"}
 
 
+def bench_workload_steps(dev, name="bf16_ragged_b128_m2048", reps=5):
+    """Side measurement: one full decode (every step t) of another workload,
+    cross-attention and fused append + self-attention timed per call with HIP
+    events (medians over `reps` repeats; the calls are idempotent), with their
+    roofline fractions on the same algorithmic counts as the headline line."""
+    import torch
+    from paper_2608_00938_amd import grace as G
+    from paper_2608_00938_amd import workloads as W
+    wl = W.WORKLOADS[name]
+    inp = W.DecodeInputs(wl, 0, dev)
+    ek, ev_ = inp.enc_kv
+    off = inp.offsets_tensor()
+    scale = 1.0 / math.sqrt(wl.d)
+    parents_np = [inp.parents(t) for t in range(wl.steps)]
+    cross_flops, _, _, _, _, fused_b = algorithmic(wl, inp.sum_L, parents_np)
+    cache = G.KVCache(wl.B, wl.M, wl.H, wl.d, wl.steps, wl.torch_dtype, dev)
+    xc = torch.empty((wl.R, wl.H, wl.d), dtype=wl.torch_dtype, device=dev)
+    xs = torch.empty_like(xc)
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    cross_us, fused_us = [], []
+    for t in range(wl.steps):
+        qc, qs = inp.step_tensor("q_cross", t), inp.step_tensor("q_self", t)
+        kn, vn = inp.step_tensor("k_new", t), inp.step_tensor("v_new", t)
+        par = None if parents_np[t] is None else torch.from_numpy(parents_np[t]).to(dev)
+        tc, tf = [], []
+        for _ in range(reps + 1):
+            e[0].record()
+            G.grace_cross_attn(qc, ek, ev_, off, wl.M, scale, out=xc)
+            e[1].record()
+            cache.append_attend(t, qs, kn, vn, par, scale, out=xs)
+            e[2].record()
+            torch.cuda.synchronize()
+            tc.append(e[0].elapsed_time(e[1]) * 1e3)
+            tf.append(e[1].elapsed_time(e[2]) * 1e3)
+        cross_us.append(float(np.median(tc[1:])))
+        fused_us.append(float(np.median(tf[1:])))
+        del qc, qs, kn, vn
+    c_mean, f_mean = float(np.mean(cross_us)), float(np.mean(fused_us))
+    f_bytes = float(np.mean(fused_b))
+    return {"workload": name, "requests": wl.B, "beams": wl.M, "sum_L": inp.sum_L,
+            "heads": wl.H, "head_dim": wl.d, "decode_steps": wl.steps,
+            "us_per_step": round(c_mean + f_mean, 1),
+            "cross_attn_us": round(c_mean, 1),
+            "cross_attn_mfma_frac": round(cross_flops / (c_mean * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "self_attn_fused_us": round(f_mean, 1),
+            "self_attn_fused_by_step_us": [round(x, 1) for x in fused_us],
+            "self_attn_fused_hbm_frac": round(f_bytes / (f_mean * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+            "note": "side measurement, not part of value"}
+
+
 def torch_index(a):
     import torch
     return torch.from_numpy(np.ascontiguousarray(a))
@@ -429,6 +479,8 @@ def main():
         result["beam_step"] = bench_beam_step(wl, dev)
         result["decode_loop_graph"] = bench_decode_loop(dev)
         result["gtm_filter"] = bench_gtm(wl, dev)
+        result["other_workloads"] = [bench_workload_steps(dev, n)
+                                     for n in ("bf16_b32_m1024", "bf16_ragged_b128_m2048")]
     if not args.no_cpu_baseline:
         log("timing the oracle on host cores ...")
         result["cpu_baseline"] = cpu_baseline(wl, inp, parents_np)

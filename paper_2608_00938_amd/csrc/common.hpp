@@ -93,4 +93,15 @@ __device__ __forceinline__ float group_sum(float x) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// XCD-aware workgroup order.  Consecutive workgroup ids go round-robin over
+// the 8 XCDs; the remapped index i' gives XCD x the contiguous range
+// [x*n/8, (x+1)*n/8), processed in order, so that work items that share data
+// (the beam tiles of one request and head, or the beam rows of one request)
+// run on one XCD and close in time, and that XCD's L2 serves them all.
+__device__ __forceinline__ uint32_t xcd_remap(uint32_t i, uint32_t n) {
+  constexpr uint32_t kXcds = 8;
+  if (n % kXcds != 0) return i;
+  return (i % kXcds) * (n / kXcds) + i / kXcds;
+}
+
 }  // namespace grace

@@ -28,17 +28,6 @@
 
 namespace grace {
 
-// ---------------------------------------------------------------------------
-// XCD-aware tile order.  Consecutive workgroup ids go round-robin over the 8
-// XCDs; remapping puts the beam tiles of one (request, head) on one XCD and
-// close in time, so that XCD's L2 serves the request's K/V to all of them.
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ uint32_t xcd_remap(uint32_t i, uint32_t n) {
-  constexpr uint32_t kXcds = 8;
-  if (n % kXcds != 0) return i;
-  return (i % kXcds) * (n / kXcds) + i / kXcds;
-}
-
 __device__ __forceinline__ void request_span(const int32_t* off, int32_t b, int32_t sum_L,
                                              int32_t& o0, int32_t& L) {
   int32_t a = off[b], e = off[b + 1];

@@ -144,7 +144,7 @@ self_attn_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_pool,
                  const u32x4* __restrict__ v_pool, const int32_t* __restrict__ table,
                  u32x4* __restrict__ out, int64_t total_chunks, int32_t chunks_per_row,
                  int32_t T_max, uint32_t nblocks, float c_scale) {
-  const int64_t g = (int64_t)blockIdx.x * kSelfThreads + threadIdx.x;
+  const int64_t g = (int64_t)xcd_remap(blockIdx.x, gridDim.x) * kSelfThreads + threadIdx.x;
   if (g >= total_chunks) return;   // wave-uniform when UNIFORM (rows are whole waves)
   const int64_t r = row_of<UNIFORM>(g, chunks_per_row);
   const int32_t c = (int32_t)(g - r * chunks_per_row);
@@ -176,7 +176,7 @@ self_attn_fused_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_
                        float c_scale, int32_t copy_k, int32_t copy_v,
                        int32_t* __restrict__ err_flag) {
   constexpr int STEP = NT - 1;
-  const int64_t g = (int64_t)blockIdx.x * kSelfThreads + threadIdx.x;
+  const int64_t g = (int64_t)xcd_remap(blockIdx.x, gridDim.x) * kSelfThreads + threadIdx.x;
   if (g >= total_chunks) return;   // wave-uniform when UNIFORM (rows are whole waves)
   const int64_t r = row_of<UNIFORM>(g, chunks_per_row);
   const int32_t c = (int32_t)(g - r * chunks_per_row);
