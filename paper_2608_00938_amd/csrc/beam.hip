@@ -354,6 +354,25 @@ topk_slice_hist_kernel(const float* __restrict__ cand, int32_t M, int32_t V, Top
   for (int i = threadIdx.x; i < kHistBins; i += kSliceThreads) out[i] = hist[i];
 }
 
+// Sum of the slice histograms of a request, bins [256 p, 256 p + 256) per
+// workgroup, written over slice 0's histogram (each bin is read and written by
+// one thread only).
+constexpr int kReduceBins = 256;
+__global__ void __launch_bounds__(kReduceBins)
+topk_hist_reduce_kernel(TopkWs ws) {
+  const int64_t b = blockIdx.y;
+  const int bin = blockIdx.x * kReduceBins + threadIdx.x;
+  uint32_t* h = ws.hist + b * ws.S * (int64_t)kHistBins + bin;
+  // eight slices in flight per thread
+  uint32_t part[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+  int j = 0;
+  for (; j + 8 <= ws.S; j += 8)
+#pragma unroll
+    for (int u = 0; u < 8; ++u) part[u] += h[(int64_t)(j + u) * kHistBins];
+  for (; j < ws.S; ++j) part[0] += h[(int64_t)j * kHistBins];
+  h[0] = ((part[0] + part[1]) + (part[2] + part[3])) + ((part[4] + part[5]) + (part[6] + part[7]));
+}
+
 __global__ void __launch_bounds__(kTopkThreads)
 topk_boundary_kernel(int32_t k, TopkWs ws) {
   __shared__ uint32_t scan[64];
@@ -364,10 +383,9 @@ topk_boundary_kernel(int32_t k, TopkWs ws) {
   // thread 0 owns the top 4 bins, in descending order
   const int t_rev = kTopkThreads - 1 - tid;
   uint32_t own[4] = {0u, 0u, 0u, 0u}, s4 = 0;
-  const uint32_t* h = ws.hist + b * ws.S * (int64_t)kHistBins;
-  for (int j = 0; j < ws.S; ++j)
+  const uint32_t* h = ws.hist + b * ws.S * (int64_t)kHistBins;   // the request's total
 #pragma unroll
-    for (int e = 0; e < 4; ++e) own[e] += h[(int64_t)j * kHistBins + 4 * t_rev + 3 - e];
+  for (int e = 0; e < 4; ++e) own[e] = h[4 * t_rev + 3 - e];
 #pragma unroll
   for (int e = 0; e < 4; ++e) s4 += own[e];
   __syncthreads();
@@ -623,6 +641,8 @@ hipError_t launch_beam_topk(const float* cand, const float* row_max, int32_t B, 
                      M, V, ws);
   hipLaunchKernelGGL(topk_slice_hist_kernel, slices, dim3(kSliceThreads), 0, stream, cand, M, V,
                      ws);
+  hipLaunchKernelGGL(topk_hist_reduce_kernel, dim3(kHistBins / kReduceBins, (unsigned)B),
+                     dim3(kReduceBins), 0, stream, ws);
   hipLaunchKernelGGL(topk_boundary_kernel, dim3((unsigned)B), dim3(kTopkThreads), 0, stream, k,
                      ws);
   hipLaunchKernelGGL(topk_gather_kernel, slices, dim3(kSliceThreads), 0, stream, cand, M, V, ws);
