@@ -244,6 +244,59 @@ def bench_decode_loop(dev, name="bf16_b8_m256", layers=3, reps=20):
             "graph_us": round(graph, 1), "note": "side measurement, not part of value"}
 
 
+def bench_context(wl, inp, dev, ek, ev, off, cross_us, reps=10):
+    """Same-box context for the cross-attention roofline: torch's flash SDPA on the
+    same problem ([B, H, M, d] copies of the step-0 queries against [B, H, L, d]
+    copies of the encoder K/V), and torch.matmul's bf16 rate at 16384^3 as the
+    practical matrix-core ceiling of a plain GEMM on this chip."""
+    import torch
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    from paper_2608_00938_amd import grace as G
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    res = {"note": "side measurement, not part of value"}
+    flops = 4.0 * wl.B * wl.H * wl.M * wl.L * wl.d
+    q = inp.step_tensor("q_cross", 0)
+    mine = G.grace_cross_attn(q, ek, ev, off, wl.M, 1.0 / math.sqrt(wl.d))
+    qh = q.view(wl.B, wl.M, wl.H, wl.d).permute(0, 2, 1, 3).contiguous()
+    kh = ek.view(wl.B, wl.L, wl.H, wl.d).permute(0, 2, 1, 3).contiguous()
+    vh = ev.view(wl.B, wl.L, wl.H, wl.d).permute(0, 2, 1, 3).contiguous()
+    del q
+    try:
+        with sdpa_kernel([SDPBackend.FLASH_ATTENTION]):
+            ref = torch.nn.functional.scaled_dot_product_attention(qh, kh, vh)
+            us = timed(lambda: torch.nn.functional.scaled_dot_product_attention(qh, kh, vh))
+        res["torch_sdpa_flash_us"] = round(us, 1)
+        res["torch_sdpa_flash_TFLOPs"] = round(flops / us / 1e6, 1)
+        res["cross_attn_speedup_vs_sdpa"] = round(us / cross_us, 3)
+        res["max_abs_diff_vs_sdpa"] = float(
+            (mine.view(wl.B, wl.M, wl.H, wl.d).permute(0, 2, 1, 3).float() - ref.float()).abs().max())
+        del ref
+    except RuntimeError as e:   # no flash backend in this torch build
+        res["torch_sdpa_flash"] = f"unavailable: {str(e).splitlines()[0][:120]}"
+    del qh, kh, vh, mine
+    n = 16384
+    a = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    b = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    us = timed(lambda: torch.matmul(a, b))
+    res["gemm_bf16_16384_TFLOPs"] = round(2.0 * n ** 3 / us / 1e6, 1)
+    res["cross_attn_frac_of_gemm"] = round(flops / cross_us / 1e6 / res["gemm_bf16_16384_TFLOPs"], 4)
+    del a, b
+    torch.cuda.empty_cache()
+    return res
+
+
 def bench_workload_steps(dev, name="bf16_ragged_b128_m2048", reps=5):
     """Side measurement: one full decode (every step t) of another workload,
     cross-attention and fused append + self-attention timed per call with HIP
@@ -476,6 +529,8 @@ def main():
     if not args.no_extras:
         del steps, cache
         torch.cuda.empty_cache()
+        if not wl.ragged:
+            result["mfma_context"] = bench_context(wl, inp, dev, ek, ev, off, cross_ms * 1e3)
         result["beam_step"] = bench_beam_step(wl, dev)
         result["decode_loop_graph"] = bench_decode_loop(dev)
         result["gtm_filter"] = bench_gtm(wl, dev)

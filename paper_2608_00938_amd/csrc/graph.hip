@@ -35,7 +35,7 @@ int32_t grace_graph_end(void* stream, void** graph_exec) {
   const hipError_t e2 = hipGraphDestroy(graph);
   if (e != hipSuccess) return graph_status(e);
   if (e2 != hipSuccess) {
-    hipGraphExecDestroy(exec);
+    (void)hipGraphExecDestroy(exec);
     return graph_status(e2);
   }
   *graph_exec = (void*)exec;

@@ -67,7 +67,8 @@ def _topk_case(gpu, cand, B, M, V, k, row_max=None):
     assert np.array_equal(sc.cpu().numpy().view(np.uint32), rs.view(np.uint32)), "scores (bitwise)"
 
 
-TOPK_SHAPES = [(3, 37, 64, 50), (2, 16, 600, 4096), (4, 200, 100, 1), (1, 3, 5, 15), (2, 64, 512, 777)]
+TOPK_SHAPES = [(3, 37, 64, 50), (2, 16, 600, 4096), (4, 200, 100, 1), (1, 3, 5, 15), (2, 64, 512, 777),
+               (2, 131, 257, 2000)]   # the last: M*V not a multiple of 4, over two slices
 
 
 @pytest.mark.parametrize("shape", TOPK_SHAPES, ids=lambda s: "x".join(map(str, s)))
