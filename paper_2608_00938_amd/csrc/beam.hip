@@ -3,7 +3,9 @@
 // scores: one wave per beam row.  The row's log-softmax over the vocabulary is
 //   added to the beam's accumulated score; filtered tokens score -inf.  The
 //   kernel also writes each row's best candidate score.
-// top-k:  one 1024-thread workgroup per request over its M*V candidates.
+// top-k:  per request, slices of its M*V candidates spread over several
+//   workgroups (maxima, histograms, gather), then one 1024-thread workgroup
+//   for the boundary bin and one for the final ranking.
 //   Candidates are totally ordered by an order-preserving 32-bit key of the
 //   score (descending; -0 == +0; NaN below -inf), then by flat index m*V + v
 //   (ascending), so the selection is unique.  Fast path: a 4096-bin histogram
@@ -13,7 +15,8 @@
 //   outside the window or the gathered set would not fit, an exact radix
 //   select on the key (four 8-bit digits) and an index-ordered collection of
 //   the tied candidates take over.  Either way the k winners are sorted by
-//   (key desc, index asc) with a bitonic sort in LDS.
+//   (key desc, index asc): ranked by a counting sort over the window bins and
+//   a comparison inside each bin, or by a bitonic sort in LDS when a bin is crowded.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -477,7 +480,22 @@ struct TopkShared {
   uint64_t list[kGatherCap];
   uint32_t scan[64];
   int32_t ipar[4];
+  // fast path: members per window bin (counted from the top bin down), then
+  // the first position of each bin in the bin-ordered list
+  uint32_t bin_count[kHistBins];
+  uint32_t bin_start[kHistBins];
+  uint32_t max_count;
 };
+
+// Bins at most this full are ranked by comparing a candidate with the other
+// members of its bin; fuller bins take the bitonic sort.
+constexpr uint32_t kRankBinCap = 512;
+
+// The score a fast-path key came from (finite scores only; -0 is read back
+// from the candidates because its key is +0's).
+__device__ __forceinline__ float key_score(uint32_t key) {
+  return __uint_as_float((key & 0x80000000u) ? (key & 0x7fffffffu) : ~key);
+}
 
 // Final selection: sort the gathered candidates (fast path), or an exact radix
 // select over all the request's candidates (fallback), then emit k in order.
@@ -496,6 +514,66 @@ topk_final_kernel(const float* __restrict__ cand, int32_t M, int32_t V, int32_t 
   if (ws.info[b * 4 + 3] != 0) {
     n_sel = (uint32_t)ws.info[b * 4 + 2];
     const uint64_t* list = ws.list + b * (int64_t)kGatherCap;
+    // ---- rank by window bin: a counting sort over the bins, then each
+    // candidate's place inside its bin from the bin's other members ----
+    constexpr int kPer = kGatherCap / kTopkThreads;
+    for (int i = tid; i < kHistBins; i += kTopkThreads) sh.bin_count[i] = 0u;
+    if (tid == 0) sh.max_count = 0u;
+    __syncthreads();
+    const float best = request_best(ws, b);
+    const float lo = best - kWindow, inv_w = (float)kHistBins / kWindow;
+    uint64_t v[kPer];
+    uint32_t rb[kPer], slot[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const uint32_t i = (uint32_t)(tid + j * kTopkThreads);
+      if (i < n_sel) {
+        v[j] = list[i];
+        // the bin the gather saw: the key is the candidate's score, exactly
+        rb[j] = (uint32_t)(kHistBins - 1 - window_bin(key_score((uint32_t)(v[j] >> 32)), lo, inv_w));
+        slot[j] = atomicAdd(&sh.bin_count[rb[j]], 1u);
+      }
+    }
+    __syncthreads();
+    {
+      uint32_t c4[4], s4 = 0, mx = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        c4[e] = sh.bin_count[4 * tid + e];
+        s4 += c4[e];
+        mx = max(mx, c4[e]);
+      }
+      if (mx > 0) atomicMax(&sh.max_count, mx);
+      uint32_t total;
+      uint32_t run = block_exclusive_scan(s4, sh.scan, &total);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        sh.bin_start[4 * tid + e] = run;
+        run += c4[e];
+      }
+    }
+    __syncthreads();
+    if (sh.max_count <= kRankBinCap) {
+#pragma unroll
+      for (int j = 0; j < kPer; ++j)
+        if ((uint32_t)(tid + j * kTopkThreads) < n_sel) sh.list[sh.bin_start[rb[j]] + slot[j]] = v[j];
+      __syncthreads();
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) {
+        if ((uint32_t)(tid + j * kTopkThreads) >= n_sel) continue;
+        const uint32_t s0 = sh.bin_start[rb[j]], n = sh.bin_count[rb[j]];
+        uint32_t pos = s0;
+        for (uint32_t e = 0; e < n; ++e) pos += sh.list[s0 + e] > v[j] ? 1u : 0u;
+        if (pos < (uint32_t)k) {
+          const uint32_t key = (uint32_t)(v[j] >> 32), idx = ~(uint32_t)(v[j] & 0xffffffffull);
+          parents[b * k + pos] = (int32_t)(idx / (uint32_t)V);
+          tokens[b * k + pos] = (int32_t)(idx % (uint32_t)V);
+          scores[b * k + pos] = key == 0x80000000u ? c[idx] : key_score(key);
+        }
+      }
+      return;
+    }
+    // a crowded bin: the bitonic sort below
     for (uint32_t i = tid; i < n_sel; i += kTopkThreads) sh.list[i] = list[i];
     __syncthreads();
   } else {
