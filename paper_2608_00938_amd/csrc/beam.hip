@@ -317,10 +317,11 @@ topk_slice_max_kernel(const float* __restrict__ cand, const float* __restrict__ 
   if (threadIdx.x == 0) ws.smax[b * ws.S + s] = best;
 }
 
+// The request's best score: the maximum of its slice maxima (S <= 64, one per
+// lane), in every lane of the calling wave.
 __device__ __forceinline__ float request_best(const TopkWs& ws, int64_t b) {
-  float best = -INFINITY;
-  for (int j = 0; j < ws.S; ++j) best = fmaxf(best, ws.smax[b * ws.S + j]);
-  return best;
+  const int lane = threadIdx.x & 63;
+  return wave_max(lane < ws.S ? ws.smax[b * ws.S + lane] : -INFINITY);
 }
 
 __global__ void __launch_bounds__(kSliceThreads)
@@ -408,8 +409,8 @@ topk_boundary_kernel(int32_t k, TopkWs ws) {
     }
   }
   __syncthreads();
+  const float best = request_best(ws, b);   // whole waves
   if (tid == 0) {
-    const float best = request_best(ws, b);
     const bool finite = best == best && best > -INFINITY && best < INFINITY;
     const bool fast = finite && total >= (uint32_t)k && par[0] > 0;
     ws.info[b * 4 + 0] = par[0];
