@@ -297,15 +297,17 @@ def bench_context(wl, inp, dev, ek, ev, off, cross_us, reps=10):
     return res
 
 
-def bench_workload_steps(dev, name="bf16_ragged_b128_m2048", reps=5):
+def bench_workload_steps(dev, name="bf16_ragged_b128_m2048", reps=5, wl=None, flush_mib=0):
     """Side measurement: one full decode (every step t) of another workload,
     cross-attention and fused append + self-attention timed per call with HIP
     events (medians over `reps` repeats; the calls are idempotent), with their
-    roofline fractions on the same algorithmic counts as the headline line."""
+    roofline fractions on the same algorithmic counts as the headline line.
+    With flush_mib > 0 a buffer of that size is overwritten before every timed
+    call (outside the events), so that the inputs start outside the caches."""
     import torch
     from paper_2608_00938_amd import grace as G
     from paper_2608_00938_amd import workloads as W
-    wl = W.WORKLOADS[name]
+    wl = W.WORKLOADS[name] if wl is None else wl
     inp = W.DecodeInputs(wl, 0, dev)
     ek, ev_ = inp.enc_kv
     off = inp.offsets_tensor()
@@ -315,7 +317,8 @@ def bench_workload_steps(dev, name="bf16_ragged_b128_m2048", reps=5):
     cache = G.KVCache(wl.B, wl.M, wl.H, wl.d, wl.steps, wl.torch_dtype, dev)
     xc = torch.empty((wl.R, wl.H, wl.d), dtype=wl.torch_dtype, device=dev)
     xs = torch.empty_like(xc)
-    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    scratch = torch.empty((flush_mib << 20,), dtype=torch.uint8, device=dev) if flush_mib else None
     cross_us, fused_us = [], []
     for t in range(wl.steps):
         qc, qs = inp.step_tensor("q_cross", t), inp.step_tensor("q_self", t)
@@ -323,20 +326,27 @@ def bench_workload_steps(dev, name="bf16_ragged_b128_m2048", reps=5):
         par = None if parents_np[t] is None else torch.from_numpy(parents_np[t]).to(dev)
         tc, tf = [], []
         for _ in range(reps + 1):
+            if scratch is not None:
+                scratch.fill_(1)
             e[0].record()
             G.grace_cross_attn(qc, ek, ev_, off, wl.M, scale, out=xc)
             e[1].record()
-            cache.append_attend(t, qs, kn, vn, par, scale, out=xs)
+            if scratch is not None:
+                scratch.fill_(1)
             e[2].record()
+            cache.append_attend(t, qs, kn, vn, par, scale, out=xs)
+            e[3].record()
             torch.cuda.synchronize()
             tc.append(e[0].elapsed_time(e[1]) * 1e3)
-            tf.append(e[1].elapsed_time(e[2]) * 1e3)
+            tf.append(e[2].elapsed_time(e[3]) * 1e3)
         cross_us.append(float(np.median(tc[1:])))
         fused_us.append(float(np.median(tf[1:])))
         del qc, qs, kn, vn
     c_mean, f_mean = float(np.mean(cross_us)), float(np.mean(fused_us))
     f_bytes = float(np.mean(fused_b))
-    return {"workload": name, "requests": wl.B, "beams": wl.M, "sum_L": inp.sum_L,
+    del scratch
+    return {"workload": wl.name, "requests": wl.B, "beams": wl.M, "sum_L": inp.sum_L,
+            "caches": f"cold ({flush_mib} MiB overwritten before each call)" if flush_mib else "warm",
             "heads": wl.H, "head_dim": wl.d, "decode_steps": wl.steps,
             "us_per_step": round(c_mean + f_mean, 1),
             "cross_attn_us": round(c_mean, 1),
@@ -534,8 +544,17 @@ def main():
         result["beam_step"] = bench_beam_step(wl, dev)
         result["decode_loop_graph"] = bench_decode_loop(dev)
         result["gtm_filter"] = bench_gtm(wl, dev)
-        result["other_workloads"] = [bench_workload_steps(dev, n)
-                                     for n in ("bf16_b32_m1024", "bf16_ragged_b128_m2048")]
+        result["other_workloads"] = [bench_workload_steps(dev, n, flush_mib=f)
+                                     for n in ("bf16_b8_m256", "bf16_b32_m1024") for f in (0, 512)]
+        result["other_workloads"].append(bench_workload_steps(dev, "bf16_ragged_b128_m2048"))
+        from paper_2608_00938_amd import workloads as W
+        paper = bench_workload_steps(dev, W.PAPER_SHAPE.name, wl=W.PAPER_SHAPE)
+        # the paper's GH200 timings of this shape (cross-attention with the
+        # beam-as-query layout under FlashAttention-2/3; the fused and paged
+        # Triton self-attention at t = 0..3), for context only
+        paper["paper_gh200_us"] = {"cross_attn_fa2": 97.0, "cross_attn_fa3": 101.0,
+                                   "self_attn_paged_by_step": [216.0, 224.0, 233.0, 238.0]}
+        result["other_workloads"].append(paper)
     if not args.no_cpu_baseline:
         log("timing the oracle on host cores ...")
         result["cpu_baseline"] = cpu_baseline(wl, inp, parents_np)

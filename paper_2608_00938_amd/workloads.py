@@ -101,6 +101,12 @@ WORKLOADS = {
                                        parents="zipf", zipf_s=1.2),
 }
 
+# The paper's own microbenchmark shape (16 requests x 1024 beams, 128 encoder
+# tokens, 16 heads x 128, prefixes of t+1 tokens for t = 0..3); measured beside
+# the five workloads for comparison with the paper's GH200 timings.
+PAPER_SHAPE = Workload("bf16_paper_b16_m1024", BF16, B=16, M=1024, H=16, d=128, steps=4, L=128,
+                       parents="uniform")
+
 
 def custom(name: str = "custom", **kw) -> Workload:
     """A workload of arbitrary shape (tests use it for edge cases)."""
