@@ -122,17 +122,17 @@ __device__ __forceinline__ int tile_swizzle(int row) {
 
 // One 16-byte direct global -> LDS load per lane (global_load_lds_dwordx4):
 // lane reads base + byte_off and the wave's 64 chunks land contiguously at LDS
-// byte address lds_wave_addr + 16 * lane.  base and lds_wave_addr must be
+// byte address lds_wave_addr + 16 * lane (passed in m0).  base and lds_wave_addr must be
 // wave-uniform (scalar registers).  Issued as inline asm so that the compiler
 // neither waits for it before unrelated LDS reads nor drains it at every
 // barrier: the kernel waits for these loads explicitly (wait_vmem_upto) right
 // before the barrier that publishes the tile they fill.
 __device__ __forceinline__ void load_to_lds(const void* base, uint32_t byte_off,
                                             uint32_t lds_wave_addr) {
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+  asm volatile("global_load_lds_dwordx4 %0, %1"
                :
-               : "v"(byte_off), "s"(base), "s"(lds_wave_addr)
-               : "memory", "m0");
+               : "v"(byte_off), "s"(base), "{m0}"(lds_wave_addr)
+               : "memory");
 }
 
 // Workgroup barrier that orders LDS only: pending LDS operations complete,
@@ -493,6 +493,13 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
     const int late = prologue_late();
     wait_vmem_upto(late);   // K(0), K(1), V(0) have landed
     lds_barrier();
+    // Every scalar and LDS load issued so far is complete; saying so in a
+    // form the compiler tracks (s_waitcnt with vmcnt and expcnt at their
+    // maxima, lgkmcnt 0) lets it wait for exactly the LDS reads each product
+    // needs in the loop below.  Otherwise a scalar load it still counts as
+    // pending (it may return out of order) makes it wait for every
+    // outstanding LDS read, the ones just issued included, once per step.
+    __builtin_amdgcn_s_waitcnt(0xC07F);
 
 
     // Step j (parity P): K of step j+1 from buffer kbuf (32-key step ksub of
