@@ -167,6 +167,22 @@ def test_workload_sampled_parity(gpu, name, fused):
     assert torch.equal(dec.steps[0]["xs"], dec.steps[0]["vn"])
 
 
+@pytest.mark.parametrize("fused", [False, True], ids=["split", "fused"])
+def test_paper_shape_sampled_parity(gpu, fused):
+    """The paper's microbenchmark shape (16 x 1024 beams, 128 encoder tokens,
+    16 heads x 128) that the benchmark times beside the paper's own figures."""
+    wl = W.PAPER_SHAPE
+    _log(f"[parity sampled] {wl.name} seed=0 fused={fused}")
+    dec = Decode(wl, 0, gpu, fused)
+    for t in range(wl.steps):
+        dec.run_step(t)
+    torch.cuda.synchronize()
+    assert int(dec.cache.err_flag.item()) == 0
+    _sampled_check(dec, np.random.default_rng(1))
+    for rec in dec.steps:
+        assert bool(torch.isfinite(rec["xc"]).all()) and bool(torch.isfinite(rec["xs"]).all())
+
+
 EDGE = [
     # ragged tails: beams not a multiple of the 256-beam tile, keys not of the 64-token tile
     dict(dtype="bf16", B=3, M=300, H=3, d=64, steps=3, L_lo=1, L_hi=130),
