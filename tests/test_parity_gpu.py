@@ -210,6 +210,39 @@ def test_edge_shapes_full_parity(gpu, i, fused):
     _full_check(dec)
 
 
+def _random_shape(i):
+    """Seeded random small workload: any dtype, head dim, ragged or fixed encoder
+    lengths (including tails shorter than a key tile), beam counts off the tile
+    sizes, uniform or Zipf parents."""
+    rng = np.random.default_rng(1000 + i)
+    dtype = "f32" if i % 4 == 3 else "bf16"
+    d = int(rng.choice([32, 64, 128]))
+    kw = dict(dtype=dtype, B=int(rng.integers(1, 5)), M=int(rng.integers(1, 700)),
+              H=int(rng.integers(1, 4)), d=d, steps=int(rng.integers(1, 9)))
+    if rng.random() < 0.5:
+        kw.update(L_lo=int(rng.integers(1, 40)), L_hi=int(rng.integers(40, 300)))
+    else:
+        kw.update(L=int(rng.integers(1, 300)))
+    if rng.random() < 0.5:
+        kw.update(parents="zipf", zipf_s=float(rng.uniform(0.8, 1.6)))
+    else:
+        kw.update(parents="uniform")
+    return kw
+
+
+@pytest.mark.parametrize("fused", [False, True], ids=["split", "fused"])
+@pytest.mark.parametrize("i", range(10))
+def test_random_shapes_full_parity(gpu, i, fused):
+    kw = _random_shape(i)
+    wl = W.custom(name=f"random{i}", **kw)
+    _log(f"[parity random] {wl} fused={fused}")
+    dec = Decode(wl, 50 + i, gpu, fused)
+    for t in range(wl.steps):
+        dec.run_step(t)
+    torch.cuda.synchronize()
+    _full_check(dec)
+
+
 def test_first_step_is_v_new_bitwise(gpu):
     for dtype in ("bf16", "f32"):
         wl = W.custom(dtype=dtype, B=2, M=40, H=3, d=64, steps=2, L=8)
