@@ -93,6 +93,28 @@ __device__ __forceinline__ float group_sum(float x) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Unsigned 32-bit division by a divisor fixed for a whole launch (1 <= d <=
+// 2^31), as one high multiply, a subtract, an add and two shifts (Granlund and
+// Montgomery, "Division by invariant integers using multiplication", PLDI 1994,
+// Sec. 4): with l = ceil(log2 d) and m = floor(2^32 (2^l - d) / d) + 1,
+// n / d = (t + ((n - t) >> min(l, 1))) >> max(l - 1, 0) where t = mulhi(m, n).
+// The constants are computed on the host.
+struct FastDiv {
+  uint32_t m = 1, s1 = 0, s2 = 0;
+  FastDiv() = default;
+  __host__ explicit FastDiv(uint32_t d) {
+    uint32_t l = 0;
+    while (l < 32 && (1ull << l) < d) ++l;
+    m = (uint32_t)(((1ull << 32) * ((1ull << l) - d)) / d + 1);
+    s1 = l < 1 ? l : 1;
+    s2 = l < 1 ? 0 : l - 1;
+  }
+  __device__ __forceinline__ uint32_t div(uint32_t n) const {
+    const uint32_t t = __umulhi(m, n);
+    return (t + ((n - t) >> s1)) >> s2;
+  }
+};
+
 // XCD-aware workgroup order.  Consecutive workgroup ids go round-robin over
 // the 8 XCDs; the remapped index i' gives XCD x the contiguous range
 // [x*n/8, (x+1)*n/8), processed in order, so that work items that share data

@@ -126,33 +126,30 @@ __device__ __forceinline__ u32x4 attend_chunk(const u32x4& qc, const u32x4* kc, 
   return Chunk<T>::pack(o);
 }
 
-// Row of chunk g; wave-uniform (scalar) when rows are whole waves.
+// Row of chunk g (g / chunks_per_row); computed once per wave, in scalar
+// registers, when rows are whole waves.  Chunk and row indices fit 32 bits:
+// the entry points bound R*H*d below 2^31.
 template <bool UNIFORM>
-__device__ __forceinline__ int64_t row_of(int64_t g, int32_t chunks_per_row) {
-  const int64_t r = g / chunks_per_row;
-  if constexpr (UNIFORM) {
-    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)r);
-    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(r >> 32));
-    return (int64_t)(((uint64_t)hi << 32) | lo);
-  }
-  return r;
+__device__ __forceinline__ uint32_t row_of(uint32_t g, const FastDiv& per_row) {
+  if constexpr (UNIFORM) return per_row.div(__builtin_amdgcn_readfirstlane(g));
+  return per_row.div(g);
 }
 
 template <class T, int D, int NT, bool UNIFORM>
 __global__ void __launch_bounds__(kSelfThreads)
 self_attn_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_pool,
                  const u32x4* __restrict__ v_pool, const int32_t* __restrict__ table,
-                 u32x4* __restrict__ out, int64_t total_chunks, int32_t chunks_per_row,
-                 int32_t T_max, uint32_t nblocks, float c_scale) {
-  const int64_t g = (int64_t)xcd_remap(blockIdx.x, gridDim.x) * kSelfThreads + threadIdx.x;
+                 u32x4* __restrict__ out, uint32_t total_chunks, int32_t chunks_per_row,
+                 FastDiv per_row, int32_t T_max, uint32_t nblocks, float c_scale) {
+  const uint32_t g = xcd_remap(blockIdx.x, gridDim.x) * kSelfThreads + threadIdx.x;
   if (g >= total_chunks) return;   // wave-uniform when UNIFORM (rows are whole waves)
-  const int64_t r = row_of<UNIFORM>(g, chunks_per_row);
-  const int32_t c = (int32_t)(g - r * chunks_per_row);
+  const uint32_t r = row_of<UNIFORM>(g, per_row);
+  const int32_t c = (int32_t)(g - r * (uint32_t)chunks_per_row);
   u32x4 kc[NT], vc[NT];
   const u32x4 qc = __builtin_nontemporal_load(&q[g]);
 #pragma unroll
   for (int j = 0; j < NT; ++j) {
-    uint32_t id = (uint32_t)table[r * T_max + j];
+    uint32_t id = (uint32_t)table[(int64_t)r * T_max + j];
     id = id < nblocks ? id : nblocks - 1;
     const int64_t off = (int64_t)id * chunks_per_row + c;
     kc[j] = k_pool[off];
@@ -171,15 +168,15 @@ self_attn_fused_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_
                        const u32x4* __restrict__ v_new, u32x4* __restrict__ k_pool,
                        u32x4* __restrict__ v_pool, const int32_t* __restrict__ table_prev,
                        int32_t* __restrict__ table_next, const int32_t* __restrict__ parents,
-                       u32x4* __restrict__ out, int64_t total_chunks, int32_t chunks_per_row,
-                       int32_t R_s, int32_t M, int32_t M_prev, int32_t T_max, uint32_t nblocks,
-                       float c_scale, int32_t copy_k, int32_t copy_v,
-                       int32_t* __restrict__ err_flag) {
+                       u32x4* __restrict__ out, uint32_t total_chunks, int32_t chunks_per_row,
+                       FastDiv per_row, FastDiv per_request, int32_t R_s, int32_t M_prev,
+                       int32_t T_max, uint32_t nblocks, float c_scale, int32_t copy_k,
+                       int32_t copy_v, int32_t* __restrict__ err_flag) {
   constexpr int STEP = NT - 1;
-  const int64_t g = (int64_t)xcd_remap(blockIdx.x, gridDim.x) * kSelfThreads + threadIdx.x;
+  const uint32_t g = xcd_remap(blockIdx.x, gridDim.x) * kSelfThreads + threadIdx.x;
   if (g >= total_chunks) return;   // wave-uniform when UNIFORM (rows are whole waves)
-  const int64_t r = row_of<UNIFORM>(g, chunks_per_row);
-  const int32_t c = (int32_t)(g - r * chunks_per_row);
+  const uint32_t r = row_of<UNIFORM>(g, per_row);
+  const int32_t c = (int32_t)(g - r * (uint32_t)chunks_per_row);
 
   u32x4 kc[NT], vc[NT];
   int32_t ids[NT > 1 ? NT - 1 : 1];
@@ -192,7 +189,8 @@ self_attn_fused_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_
       if (err_flag) *err_flag = 1;
       p = p < 0 ? 0 : M_prev - 1;
     }
-    const int64_t src = (r / M) * M_prev + p;   // the parent's row among B*M_prev
+    // the parent's row among B*M_prev (request r / M)
+    const int64_t src = (int64_t)per_request.div(r) * M_prev + p;
 #pragma unroll
     for (int j = 0; j < STEP; ++j) {
       uint32_t id = (uint32_t)table_prev[src * T_max + j];
@@ -213,7 +211,7 @@ self_attn_fused_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_
 #pragma unroll
     for (int i = 0; i < STEP; ++i)
       if (j == i) id = ids[i];
-    table_next[r * T_max + j] = id;
+    table_next[(int64_t)r * T_max + j] = id;
   }
 
   __builtin_nontemporal_store(attend_chunk<T, D, NT>(qc, kc, vc, c_scale), &out[g]);
@@ -229,7 +227,7 @@ struct SelfArgs {
   int32_t* table_next;
   const int32_t* parents;
   void* out;
-  int64_t total_chunks;
+  uint32_t total_chunks;
   int32_t chunks_per_row, R, M, M_prev, T_max;
   uint32_t nblocks;
   float c_scale;
@@ -247,13 +245,14 @@ static hipError_t launch_self_nt(const SelfArgs& a, hipStream_t stream) {
                        dim3(kSelfThreads), 0, stream, (const u32x4*)a.q, (const u32x4*)a.k_new,   \
                        (const u32x4*)a.v_new, (u32x4*)a.k_pool, (u32x4*)a.v_pool, a.table_prev,   \
                        a.table_next, a.parents, (u32x4*)a.out, a.total_chunks, a.chunks_per_row,   \
-                       a.R, a.M, a.M_prev, a.T_max, a.nblocks, a.c_scale, a.copy_k, a.copy_v,      \
-                       a.err_flag);                                                                \
+                       FastDiv((uint32_t)a.chunks_per_row), FastDiv((uint32_t)a.M), a.R, a.M_prev, \
+                       a.T_max, a.nblocks, a.c_scale, a.copy_k, a.copy_v, a.err_flag);             \
   } else {                                                                                        \
     hipLaunchKernelGGL((self_attn_kernel<T, D, NT, UNI>), dim3((unsigned)blocks),                 \
                        dim3(kSelfThreads), 0, stream, (const u32x4*)a.q, (const u32x4*)a.k_pool,  \
                        (const u32x4*)a.v_pool, a.table_prev, (u32x4*)a.out, a.total_chunks,        \
-                       a.chunks_per_row, a.T_max, a.nblocks, a.c_scale);                          \
+                       a.chunks_per_row, FastDiv((uint32_t)a.chunks_per_row), a.T_max, a.nblocks, \
+                       a.c_scale);                                                                \
   }
   if (uniform) {
     GRACE_GO(true)
@@ -304,7 +303,7 @@ hipError_t launch_self_attn_step(const void* q, const void* k_pool, const void* 
   a.table_prev = table;
   a.out = out;
   a.chunks_per_row = H * d * elem / 16;
-  a.total_chunks = (int64_t)R * a.chunks_per_row;
+  a.total_chunks = (uint32_t)((int64_t)R * a.chunks_per_row);   // below 2^29: R*H*d < 2^31
   a.R = R;
   a.T_max = T_max;
   a.nblocks = (uint32_t)((int64_t)T_max * R);
@@ -330,7 +329,7 @@ hipError_t launch_self_attn_fused(const void* q, const void* k_new, const void* 
   a.parents = parents;
   a.out = out;
   a.chunks_per_row = H * d * elem / 16;
-  a.total_chunks = (int64_t)R * a.chunks_per_row;   // R = B*M rows written this step
+  a.total_chunks = (uint32_t)((int64_t)R * a.chunks_per_row);   // R = B*M rows written this step
   a.R = R_s;                                        // slab row stride of the pools
   a.M = M;
   a.M_prev = M_prev;
