@@ -17,7 +17,10 @@
 //   l += 1^T P^T          the row sums of the applied bf16 weights, on the
 //                         matrix core as well.
 // The transposed orientation puts one beam per lane column in every product,
-// so the probabilities never leave registers.
+// so the probabilities never leave registers.  Q enters and O leaves through
+// LDS as whole beam rows (direct-to-LDS loads, 16-byte row-major stores), so
+// every global access instruction covers full rows instead of 16-byte pieces
+// of 32 rows.
 //
 // fp32 path (VALU, cross_attn_f32_kernel).  One lane per beam, K/V tiles in LDS
 // read as broadcasts, fp32 FMAs throughout.
@@ -344,11 +347,13 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
     wait_vmem_upto(issued);
     lds_barrier();
   };
-  // The prologue's loads: K(0), K(1), V(0) now, K(2), V(1) after the queries.
-  auto prologue_early = [&]() __attribute__((always_inline)) {
+  // The prologue's loads: K(0), K(1), V(0) with the queries, K(2), V(1)
+  // once the queries are in registers.  Returns how many this thread issued.
+  auto prologue_early = [&]() __attribute__((always_inline)) -> int {
     if (n > 0) issue(kreq, kb_addr, 0);
     if (n > 1) issue(kreq, kb_addr, 1);
     if (n > 0) issue(vreq, vb_addr, 0);
+    return (n > 0 ? 2 : 0) * C::kLoads + (n > 1 ? C::kLoads : 0);
   };
   auto prologue_late = [&]() __attribute__((always_inline)) -> int {
     int late = 0;
@@ -357,27 +362,52 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
     return late;
   };
 
-  prologue_early();
-
-  // Q^T fragments (B operand of S^T = K Q^T): lane holds 8 consecutive d of
-  // beam l32 of block mb, for 16-wide d step ks.  Beams past M repeat beam
-  // M-1, whose results are never stored.
-  bf16x8 qf[C::kMB][C::kKS];
+  // Queries.  Each wave copies its beams' Q rows into a staging buffer of its
+  // own (K buffer 2 or 3, V buffer 2 or 3: free until the loads that follow
+  // the prologue barrier) in the tile layout, with direct-to-LDS loads whose
+  // 64 lanes cover whole rows, then reads its Q^T fragments (B operand of
+  // S^T = K Q^T) from there: lane holds 8 consecutive d of beam l32 of block
+  // mb, for 16-wide d step ks.  Beams past M repeat beam M-1, whose results
+  // are never stored.  The queries are issued first: they are needed first.
+  char* const qbuf = wave < 2 ? kbuf0 + (2 + wave) * C::kTileBytes
+                              : vbuf0 + wave * C::kTileBytes;
+  if (active) {
+    const uint16_t* const qbase = q + __builtin_amdgcn_readfirstlane((b * M + m_base) * E + h * D);
+    const uint32_t q_lds = __builtin_amdgcn_readfirstlane(lds_addr(qbuf));
+    const int last = M - 1 - m_base;
 #pragma unroll
-  for (int mb = 0; mb < C::kMB; ++mb) {
-    int32_t m = m_base + mb * 32 + l32;
-    m = m < M ? m : M - 1;
-    const uint16_t* qrow = q + (b * M + m) * E + h * D + 8 * hi;
-#pragma unroll
-    for (int ks = 0; ks < C::kKS; ++ks) {
-      const u32x4 u = *(const u32x4*)(qrow + ks * 16);
-      float f[8];
-      Chunk<BF16>::unpack(u, f);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) f[e] *= c;
-      qf[mb][ks] = __builtin_bit_cast(bf16x8, Chunk<BF16>::pack(f));
+    for (int i = 0; i < C::kTileBytes / 1024; ++i) {
+      const int sl = i * 64 + lane;
+      const int row = sl / C::kCPR;
+      const int chunk = (sl % C::kCPR) ^ tile_swizzle<D>(row);
+      const int r = row < last ? row : last;
+      load_to_lds(qbase, (uint32_t)(r * E + chunk * 8) * 2u, q_lds + i * 1024);
     }
   }
+  const int early = prologue_early();
+  wait_vmem_upto(early);   // this wave's queries have landed
+  bf16x8 qf[C::kMB][C::kKS];
+  if (active) {
+#pragma unroll
+    for (int mb = 0; mb < C::kMB; ++mb)
+#pragma unroll
+      for (int ks = 0; ks < C::kKS; ++ks) {
+        const u32x4 u = *(const u32x4*)(qbuf + C::slot(mb * 32 + l32, 2 * ks + hi) * 16);
+        float f[8];
+        Chunk<BF16>::unpack(u, f);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] *= c;
+        qf[mb][ks] = __builtin_bit_cast(bf16x8, Chunk<BF16>::pack(f));
+      }
+  } else {
+#pragma unroll
+    for (int mb = 0; mb < C::kMB; ++mb)
+#pragma unroll
+      for (int ks = 0; ks < C::kKS; ++ks) qf[mb][ks] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+  }
+  wait_vmem_upto(0);   // K(0), K(1), V(0) have landed
+  // publishes K(0), K(1), V(0); every staging buffer has been read
+  lds_barrier();
 
   // LDS read offsets of this lane within a tile.  K (A of S^T): one per
   // 16-wide d step.  V^T (transposed reads): one per (8-row half, 32-wide d
@@ -490,9 +520,7 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
     for (int mb = 0; mb < C::kMB; ++mb)
       pf[1][mb] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
 
-    const int late = prologue_late();
-    wait_vmem_upto(late);   // K(0), K(1), V(0) have landed
-    lds_barrier();
+    prologue_late();
     // Every scalar and LDS load issued so far is complete; saying so in a
     // form the compiler tracks (s_waitcnt with vmcnt and expcnt at their
     // maxima, lgkmcnt 0) lets it wait for exactly the LDS reads each product
@@ -765,26 +793,62 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
     }
   }
 
+  // Output.  Each wave normalises its O^T, writes it to V buffer `wave` as
+  // beam-major rows in the tile layout, and stores whole rows from there: a
+  // store instruction then writes 64 16-byte chunks that cover full rows
+  // rather than 32 scattered 16-byte pieces.  Every wave is past the barrier
+  // after its last LDS read (the vote's, or the safe pass's last tile), every
+  // tile load has landed, and no wave touches another wave's buffer here.
   if (active) {
+    char* const obuf = vbuf0 + wave * C::kTileBytes;
+    // lane index opaque to the compiler, so that the addresses below are not
+    // hoisted above the main loop (where they would only occupy registers)
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int l32e = ln & 31, hie = ln >> 5;
 #pragma unroll
     for (int mb = 0; mb < C::kMB; ++mb) {
       // beam l32's row sum: lane l32 & 15, row 2mb (l32 < 16) or 2mb+1
-      const float s_lo = __shfl(lsum[2 * mb], l32 & 15);
-      const float s_hi = __shfl(lsum[2 * mb + 1], l32 & 15);
-      const float l_tot = l32 < 16 ? s_lo : s_hi;
+      const float s_lo = __shfl(lsum[2 * mb], l32e & 15);
+      const float s_hi = __shfl(lsum[2 * mb + 1], l32e & 15);
+      const float l_tot = l32e < 16 ? s_lo : s_hi;
       const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
-      const int32_t m = m_base + mb * 32 + l32;
-      if (m < M) {
-        uint16_t* dst = out + (b * M + m) * E + h * D + 4 * hi;
 #pragma unroll
-        for (int db = 0; db < C::kDB; ++db)
+      for (int db = 0; db < C::kDB; ++db)
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const u32x2 u = {pack_bf16x2(o[db][mb][4 * g + 0] * inv, o[db][mb][4 * g + 1] * inv),
-                             pack_bf16x2(o[db][mb][4 * g + 2] * inv, o[db][mb][4 * g + 3] * inv)};
-            *(u32x2*)(dst + db * 32 + 8 * g) = u;
+        for (int gp = 0; gp < 2; ++gp) {
+          // lane holds d = 32db + 16gp + {0..3} + 4hi (group 2gp) and + 8
+          // (group 2gp+1); the swap with lane l ^ 32 leaves d 32db + 16gp +
+          // 8hi + {0..7} in (a, b)
+          uint32_t a[2], c2[2];
+#pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            a[e] = pack_bf16x2(o[db][mb][8 * gp + 2 * e] * inv, o[db][mb][8 * gp + 2 * e + 1] * inv);
+            c2[e] = pack_bf16x2(o[db][mb][8 * gp + 4 + 2 * e] * inv,
+                                o[db][mb][8 * gp + 4 + 2 * e + 1] * inv);
           }
-      }
+          u32x4 chunk;
+#pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            const auto r = __builtin_amdgcn_permlane32_swap(a[e], c2[e], false, false);
+            chunk[e] = r[0];
+            chunk[2 + e] = r[1];
+          }
+          const int row = mb * 32 + l32e;
+          *(u32x4*)(obuf + C::slot(row, 4 * db + 2 * gp + hie) * 16) = chunk;
+        }
+    }
+    __builtin_amdgcn_wave_barrier();
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    constexpr int kRows = C::kMB * 32;
+    constexpr int kRowsPerPass = 64 / C::kCPR;
+#pragma unroll
+    for (int i = 0; i < kRows / kRowsPerPass; ++i) {
+      const int row = i * kRowsPerPass + ln / C::kCPR;
+      const int ch = ln % C::kCPR;
+      const u32x4 u = *(const u32x4*)(obuf + C::slot(row, ch) * 16);
+      const int32_t m = m_base + row;
+      if (m < M) *(u32x4*)(out + (b * M + m) * E + h * D + ch * 8) = u;
     }
   }
 }
