@@ -379,7 +379,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this hot path shards by request with no exchange, and "
-              f"this build runs on a single MI355X (asked for --gpus {args.gpus})", file=sys.stderr)
+              f"the benchmark times a single MI355X (asked for --gpus {args.gpus})", file=sys.stderr)
         sys.exit(2)
 
     import torch
