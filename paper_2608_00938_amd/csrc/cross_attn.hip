@@ -248,6 +248,12 @@ struct Cfg {
   __device__ __forceinline__ static int slot(int key, int chunk) {
     return key * kCPR + (chunk ^ tile_swizzle<D>(key));
   }
+  // Output staging layout: eight consecutive beam rows written at one chunk
+  // index, and one row read whole, both fall on distinct 16-byte bank groups.
+  __device__ __forceinline__ static int out_slot(int row, int chunk) {
+    const int s = kCPR >= 8 ? (row & 7) : ((row >> 1) & (kCPR - 1));
+    return row * kCPR + (chunk ^ s);
+  }
 };
 
 // s_waitcnt vmcnt(n) for n in [0, 8].
@@ -794,7 +800,7 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
   }
 
   // Output.  Each wave normalises its O^T, writes it to V buffer `wave` as
-  // beam-major rows in the tile layout, and stores whole rows from there: a
+  // beam-major rows (out_slot layout), and stores whole rows from there: a
   // store instruction then writes 64 16-byte chunks that cover full rows
   // rather than 32 scattered 16-byte pieces.  Every wave is past the barrier
   // after its last LDS read (the vote's, or the safe pass's last tile), every
@@ -835,7 +841,7 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
             chunk[2 + e] = r[1];
           }
           const int row = mb * 32 + l32e;
-          *(u32x4*)(obuf + C::slot(row, 4 * db + 2 * gp + hie) * 16) = chunk;
+          *(u32x4*)(obuf + C::out_slot(row, 4 * db + 2 * gp + hie) * 16) = chunk;
         }
     }
     __builtin_amdgcn_wave_barrier();
@@ -846,7 +852,7 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
     for (int i = 0; i < kRows / kRowsPerPass; ++i) {
       const int row = i * kRowsPerPass + ln / C::kCPR;
       const int ch = ln % C::kCPR;
-      const u32x4 u = *(const u32x4*)(obuf + C::slot(row, ch) * 16);
+      const u32x4 u = *(const u32x4*)(obuf + C::out_slot(row, ch) * 16);
       const int32_t m = m_base + row;
       if (m < M) *(u32x4*)(out + (b * M + m) * E + h * D + ch * 8) = u;
     }
