@@ -133,8 +133,10 @@ beam_scores_vec_kernel(const T* __restrict__ logits, const float* __restrict__ p
       o[e] = ((bits >> e) & 1u) ? p + (f[c][e] - lse) : -INFINITY;
       best = fmaxf(best, o[e]);
     }
-    *(u32x4*)(out + v0) = Chunk<F32>::pack(o);
-    *(u32x4*)(out + v0 + 4) = Chunk<F32>::pack(o + 4);
+    // streamed past the caches: the array is larger than L2 and MALL, and
+    // the top-k reads it back with streaming loads as well
+    __builtin_nontemporal_store(Chunk<F32>::pack(o), (u32x4*)(out + v0));
+    __builtin_nontemporal_store(Chunk<F32>::pack(o + 4), (u32x4*)(out + v0 + 4));
   }
   best = wave_max(best);
   if (row_max != nullptr && lane == 0) row_max[r] = best;
@@ -338,13 +340,14 @@ topk_slice_hist_kernel(const float* __restrict__ cand, int32_t M, int32_t V, Top
     uint32_t i0, i1;
     slice_range(N, ws.S, s, i0, i1);
     const float* c = cand + b * (int64_t)N;
-    // four candidates in flight per thread; one LDS atomic per counted candidate
+    // four candidates in flight per thread (streaming loads); one LDS atomic
+    // per counted candidate
     for (uint32_t j0 = i0; j0 < i1; j0 += 4 * kSliceThreads) {
       float x[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const uint32_t i = j0 + u * kSliceThreads + threadIdx.x;
-        x[u] = i < i1 ? c[i] : -INFINITY;
+        x[u] = i < i1 ? __builtin_nontemporal_load(&c[i]) : -INFINITY;
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -461,7 +464,7 @@ topk_gather_kernel(const float* __restrict__ cand, int32_t M, int32_t V, TopkWs 
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const uint32_t i = j0 + u * kSliceThreads + threadIdx.x;
-      x[u] = i < i1 ? c[i] : -INFINITY;
+      x[u] = i < i1 ? __builtin_nontemporal_load(&c[i]) : -INFINITY;
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
