@@ -129,13 +129,22 @@ __device__ __forceinline__ int tile_swizzle(int row) {
 // wave-uniform (scalar registers).  Issued as inline asm so that the compiler
 // neither waits for it before unrelated LDS reads nor drains it at every
 // barrier: the kernel waits for these loads explicitly (wait_vmem_upto) right
-// before the barrier that publishes the tile they fill.
+// before the barrier that publishes the tile they fill.  NT marks data read
+// once (the queries) as streaming, so that it does not displace the K/V tiles
+// that the other beam tiles of the request still read.
+template <bool NT = false>
 __device__ __forceinline__ void load_to_lds(const void* base, uint32_t byte_off,
                                             uint32_t lds_wave_addr) {
-  asm volatile("global_load_lds_dwordx4 %0, %1"
-               :
-               : "v"(byte_off), "s"(base), "{m0}"(lds_wave_addr)
-               : "memory");
+  if constexpr (NT)
+    asm volatile("global_load_lds_dwordx4 %0, %1 nt"
+                 :
+                 : "v"(byte_off), "s"(base), "{m0}"(lds_wave_addr)
+                 : "memory");
+  else
+    asm volatile("global_load_lds_dwordx4 %0, %1"
+                 :
+                 : "v"(byte_off), "s"(base), "{m0}"(lds_wave_addr)
+                 : "memory");
 }
 
 // Workgroup barrier that orders LDS only: pending LDS operations complete,
@@ -387,7 +396,7 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
       const int row = sl / C::kCPR;
       const int chunk = (sl % C::kCPR) ^ tile_swizzle<D>(row);
       const int r = row < last ? row : last;
-      load_to_lds(qbase, (uint32_t)(r * E + chunk * 8) * 2u, q_lds + i * 1024);
+      load_to_lds<true>(qbase, (uint32_t)(r * E + chunk * 8) * 2u, q_lds + i * 1024);
     }
   }
   const int early = prologue_early();
@@ -802,7 +811,8 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
   // Output.  Each wave normalises its O^T, writes it to V buffer `wave` as
   // beam-major rows (out_slot layout), and stores whole rows from there: a
   // store instruction then writes 64 16-byte chunks that cover full rows
-  // rather than 32 scattered 16-byte pieces.  Every wave is past the barrier
+  // rather than 32 scattered 16-byte pieces.  The stores are streaming: O is
+  // written once and no later access in the kernel reuses it.  Every wave is past the barrier
   // after its last LDS read (the vote's, or the safe pass's last tile), every
   // tile load has landed, and no wave touches another wave's buffer here.
   if (active) {
@@ -854,7 +864,7 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
       const int ch = ln % C::kCPR;
       const u32x4 u = *(const u32x4*)(obuf + C::out_slot(row, ch) * 16);
       const int32_t m = m_base + row;
-      if (m < M) *(u32x4*)(out + (b * M + m) * E + h * D + ch * 8) = u;
+      if (m < M) __builtin_nontemporal_store(u, (u32x4*)(out + (b * M + m) * E + h * D + ch * 8));
     }
   }
 }
