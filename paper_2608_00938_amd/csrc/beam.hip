@@ -8,10 +8,14 @@
 //   for the boundary bin and one for the final ranking.
 //   Candidates are totally ordered by an order-preserving 32-bit key of the
 //   score (descending; -0 == +0; NaN below -inf), then by flat index m*V + v
-//   (ascending), so the selection is unique.  Fast path: a 4096-bin histogram
-//   of the scores in the 64-unit window below the request's best score finds
-//   the bin holding the k-th candidate; only candidates in that bin and above
-//   are gathered into LDS and sorted exactly.  When the k-th candidate lies
+//   (ascending), so the selection is unique.  Sampled path: a 4096-bin
+//   histogram, over a sixteenth of the candidates, of the scores in the
+//   64-unit window below the request's best score picks the bin above which
+//   about 1.25 k candidates are expected; one pass gathers every candidate in
+//   that bin and above and counts them, and the set is kept when it holds at
+//   least k and fits the list.  Otherwise the full path: the same histogram
+//   over every candidate finds the bin holding the k-th candidate, and only
+//   candidates in that bin and above are gathered.  When the k-th candidate lies
 //   outside the window or the gathered set would not fit, an exact radix
 //   select on the key (four 8-bit digits) and an index-ordered collection of
 //   the tied candidates take over.  Either way the k winners are sorted by
@@ -258,8 +262,9 @@ __host__ __device__ inline int topk_slices(uint32_t N) {
 }
 
 // Workspace of one call (per request b): slice maxima [S], slice histograms
-// [S][kHistBins], info [4] = {b*, count above b*, gathered count, fast flag},
-// gathered list [kGatherCap] of composites.
+// [S][kHistBins], info [kInfo] = {b*, count above b*, gathered count, fast
+// flag, done flag, unused...}, gathered list [kGatherCap] of composites.
+constexpr int kInfo = 8;
 struct TopkWs {
   float* smax;
   uint32_t* hist;
@@ -278,7 +283,7 @@ struct TopkWs {
   }
   __host__ __device__ static size_t bytes(int B, int S_) {
     return (size_t)B * kGatherCap * 8 + (size_t)B * S_ * kHistBins * 4 + (size_t)B * S_ * 4 +
-           (size_t)B * 4 * 4;
+           (size_t)B * kInfo * 4;
   }
 };
 
@@ -331,6 +336,7 @@ topk_slice_hist_kernel(const float* __restrict__ cand, int32_t M, int32_t V, Top
   __shared__ uint32_t hist[kHistBins];
   const int s = blockIdx.x;
   const int64_t b = blockIdx.y;
+  if (ws.info[b * kInfo + 4] != 0) return;   // the sampled path succeeded
   const uint32_t N = (uint32_t)M * (uint32_t)V;
   for (int i = threadIdx.x; i < kHistBins; i += kSliceThreads) hist[i] = 0u;
   __syncthreads();
@@ -361,30 +367,92 @@ topk_slice_hist_kernel(const float* __restrict__ cand, int32_t M, int32_t V, Top
   for (int i = threadIdx.x; i < kHistBins; i += kSliceThreads) out[i] = hist[i];
 }
 
-// Sum of the slice histograms of a request, bins [256 p, 256 p + 256) per
-// workgroup, written over slice 0's histogram (each bin is read and written by
-// one thread only).
+// The sample: of every group of 16 consecutive 128-byte chunks (512
+// candidates) of a request's flat candidate array, the one chunk picked by a
+// multiplicative hash of the group index (so that neither a row's token order
+// nor the row length biases it).  A sixteenth of the candidates.
+__device__ __forceinline__ uint32_t sample_chunk(uint32_t group) {
+  return 16u * group + ((group * 0x9E3779B1u) >> 28);
+}
+
+// Histogram of the sampled candidates of kSampleGroup consecutive slices, in
+// the same window and bins as the full slice histograms (written to the
+// buffer of slice blockIdx.x; the sum then runs over the first
+// sample_slices(S) buffers).
+constexpr int kSampleGroup = 8;
+__host__ __device__ inline int sample_slices(int S) { return (S + kSampleGroup - 1) / kSampleGroup; }
+
+__global__ void __launch_bounds__(kSliceThreads)
+topk_sample_hist_kernel(const float* __restrict__ cand, int32_t M, int32_t V, TopkWs ws) {
+  __shared__ uint32_t hist[kHistBins];
+  const int s = blockIdx.x;
+  const int64_t b = blockIdx.y;
+  const uint32_t N = (uint32_t)M * (uint32_t)V;
+  for (int i = threadIdx.x; i < kHistBins; i += kSliceThreads) hist[i] = 0u;
+  __syncthreads();
+  const float best = request_best(ws, b);
+  if (best == best && best > -INFINITY && best < INFINITY) {
+    const float lo = best - kWindow, inv_w = (float)kHistBins / kWindow;
+    uint32_t i0, i1, j0, j1;
+    slice_range(N, ws.S, s * kSampleGroup, i0, j1);
+    slice_range(N, ws.S, min(s * kSampleGroup + kSampleGroup, ws.S) - 1, j0, i1);
+    const float* c = cand + b * (int64_t)N;
+    // one sampled chunk per 32-lane half-wave and group, eight groups in flight
+    const int half = threadIdx.x >> 5, l = threadIdx.x & 31;
+    constexpr int kHalves = kSliceThreads / 32;
+    const uint32_t g0 = i0 >> 9, g1 = (i1 + 511) >> 9;
+    for (uint32_t gg = g0 + half; gg < g1; gg += 8 * kHalves) {
+      float x[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t g = gg + u * kHalves;
+        const uint32_t i = 32u * sample_chunk(g) + l;
+        x[u] = g < g1 && i >= i0 && i < i1 ? __builtin_nontemporal_load(&c[i]) : -INFINITY;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int bin = window_bin(x[u], lo, inv_w);
+        if (bin > 0) atomicAdd(&hist[bin], 1u);
+      }
+    }
+  }
+  __syncthreads();
+  uint32_t* out = ws.hist + (b * ws.S + s) * (int64_t)kHistBins;
+  for (int i = threadIdx.x; i < kHistBins; i += kSliceThreads) out[i] = hist[i];
+}
+
+// Sum of the first n_slices slice histograms of a request, bins [256 p,
+// 256 p + 256) per workgroup, written over slice 0's histogram (each bin is
+// read and written by one thread only).
 constexpr int kReduceBins = 256;
 __global__ void __launch_bounds__(kReduceBins)
-topk_hist_reduce_kernel(TopkWs ws) {
+topk_hist_reduce_kernel(TopkWs ws, int32_t n_slices, int32_t skip_if_done) {
   const int64_t b = blockIdx.y;
+  if (skip_if_done && ws.info[b * kInfo + 4] != 0) return;
   const int bin = blockIdx.x * kReduceBins + threadIdx.x;
   uint32_t* h = ws.hist + b * ws.S * (int64_t)kHistBins + bin;
   // eight slices in flight per thread
   uint32_t part[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
   int j = 0;
-  for (; j + 8 <= ws.S; j += 8)
+  for (; j + 8 <= n_slices; j += 8)
 #pragma unroll
     for (int u = 0; u < 8; ++u) part[u] += h[(int64_t)(j + u) * kHistBins];
-  for (; j < ws.S; ++j) part[0] += h[(int64_t)j * kHistBins];
+  for (; j < n_slices; ++j) part[0] += h[(int64_t)j * kHistBins];
   h[0] = ((part[0] + part[1]) + (part[2] + part[3])) + ((part[4] + part[5]) + (part[6] + part[7]));
 }
 
+// SAMPLED: the histogram holds a sixteenth of the candidates.  The chosen bin
+// is the highest whose sample count from the top reaches 1.25 k / 16, so that
+// about 1.25 k candidates are expected at or above it; no fit check here, as
+// the gather counts them exactly and topk_verify_kernel decides.
+template <bool SAMPLED>
 __global__ void __launch_bounds__(kTopkThreads)
-topk_boundary_kernel(int32_t k, TopkWs ws) {
+topk_boundary_kernel(int32_t k_req, TopkWs ws) {
   __shared__ uint32_t scan[64];
   const int tid = threadIdx.x;
   const int64_t b = blockIdx.x;
+  if (!SAMPLED && ws.info[b * kInfo + 4] != 0) return;   // the sampled path succeeded
+  const int32_t k = SAMPLED ? (5 * k_req + 63) / 64 : k_req;
   __shared__ int32_t par[2];
   if (tid < 2) par[tid] = 0;
   // thread 0 owns the top 4 bins, in descending order
@@ -406,7 +474,7 @@ topk_boundary_kernel(int32_t k, TopkWs ws) {
         par[0] = 4 * t_rev + 3 - e;
         par[1] = (int32_t)run;
         // fast only if everything in bins >= b* fits the gather list
-        par[0] = (par[0] > 0 && run + own[e] <= (uint32_t)kGatherCap) ? par[0] : 0;
+        par[0] = (par[0] > 0 && (SAMPLED || run + own[e] <= (uint32_t)kGatherCap)) ? par[0] : 0;
       }
       run += own[e];
     }
@@ -416,11 +484,25 @@ topk_boundary_kernel(int32_t k, TopkWs ws) {
   if (tid == 0) {
     const bool finite = best == best && best > -INFINITY && best < INFINITY;
     const bool fast = finite && total >= (uint32_t)k && par[0] > 0;
-    ws.info[b * 4 + 0] = par[0];
-    ws.info[b * 4 + 1] = par[1];
-    ws.info[b * 4 + 2] = 0;          // gather counter
-    ws.info[b * 4 + 3] = fast ? 1 : 0;
+    ws.info[b * kInfo + 0] = par[0];
+    ws.info[b * kInfo + 1] = par[1];
+    ws.info[b * kInfo + 2] = 0;          // gather counter
+    ws.info[b * kInfo + 3] = fast ? 1 : 0;
+    if (SAMPLED) ws.info[b * kInfo + 4] = 0;   // done flag of this call
   }
+}
+
+// After the gather at the sampled bin: the gathered set holds the k best
+// exactly when at least k candidates lie at or above that bin; it is usable
+// when it also fits the list.  Otherwise the full histogram path runs.
+__global__ void __launch_bounds__(64)
+topk_verify_kernel(int32_t B, int32_t k, TopkWs ws) {
+  const int64_t b = (int64_t)blockIdx.x * 64 + threadIdx.x;
+  if (b >= B) return;
+  int32_t* info = ws.info + b * kInfo;
+  const uint32_t n = (uint32_t)info[2];
+  const bool ok = info[3] != 0 && n >= (uint32_t)k && n <= (uint32_t)kGatherCap;
+  info[4] = ok ? 1 : 0;
 }
 
 // Gathered candidates are staged in LDS and flushed to the request's list
@@ -433,15 +515,16 @@ topk_gather_kernel(const float* __restrict__ cand, int32_t M, int32_t V, TopkWs 
   __shared__ uint32_t n_stage, base;
   const int s = blockIdx.x;
   const int64_t b = blockIdx.y;
-  if (ws.info[b * 4 + 3] == 0) return;   // whole workgroup
-  const int bstar = ws.info[b * 4 + 0];
+  // whole workgroup: no fast path, or the sampled path already succeeded
+  if (ws.info[b * kInfo + 3] == 0 || ws.info[b * kInfo + 4] != 0) return;
+  const int bstar = ws.info[b * kInfo + 0];
   const uint32_t N = (uint32_t)M * (uint32_t)V;
   const float best = request_best(ws, b);
   const float lo = best - kWindow, inv_w = (float)kHistBins / kWindow;
   uint32_t i0, i1;
   slice_range(N, ws.S, s, i0, i1);
   const float* c = cand + b * (int64_t)N;
-  uint32_t* count = (uint32_t*)&ws.info[b * 4 + 2];
+  uint32_t* count = (uint32_t*)&ws.info[b * kInfo + 2];
   uint64_t* list = ws.list + b * (int64_t)kGatherCap;
   if (threadIdx.x == 0) n_stage = 0;
   __syncthreads();
@@ -515,8 +598,8 @@ topk_final_kernel(const float* __restrict__ cand, int32_t M, int32_t V, int32_t 
   if (tid < 4) sh.ipar[tid] = 0;
 
   uint32_t n_sel;
-  if (ws.info[b * 4 + 3] != 0) {
-    n_sel = (uint32_t)ws.info[b * 4 + 2];
+  if (ws.info[b * kInfo + 3] != 0) {
+    n_sel = (uint32_t)ws.info[b * kInfo + 2];
     const uint64_t* list = ws.list + b * (int64_t)kGatherCap;
     // ---- rank by window bin: a counting sort over the bins, then each
     // candidate's place inside its bin from the bin's other members ----
@@ -558,14 +641,17 @@ topk_final_kernel(const float* __restrict__ cand, int32_t M, int32_t V, int32_t 
     }
     __syncthreads();
     if (sh.max_count <= kRankBinCap) {
+      // members of a bin that starts at or past k are not among the k best
 #pragma unroll
       for (int j = 0; j < kPer; ++j)
-        if ((uint32_t)(tid + j * kTopkThreads) < n_sel) sh.list[sh.bin_start[rb[j]] + slot[j]] = v[j];
+        if ((uint32_t)(tid + j * kTopkThreads) < n_sel && sh.bin_start[rb[j]] < (uint32_t)k)
+          sh.list[sh.bin_start[rb[j]] + slot[j]] = v[j];
       __syncthreads();
 #pragma unroll
       for (int j = 0; j < kPer; ++j) {
         if ((uint32_t)(tid + j * kTopkThreads) >= n_sel) continue;
         const uint32_t s0 = sh.bin_start[rb[j]], n = sh.bin_count[rb[j]];
+        if (s0 >= (uint32_t)k) continue;
         uint32_t pos = s0;
         for (uint32_t e = 0; e < n; ++e) pos += sh.list[s0 + e] > v[j] ? 1u : 0u;
         if (pos < (uint32_t)k) {
@@ -721,12 +807,24 @@ hipError_t launch_beam_topk(const float* cand, const float* row_max, int32_t B, 
   const dim3 slices((unsigned)S, (unsigned)B);
   hipLaunchKernelGGL(topk_slice_max_kernel, slices, dim3(kSliceThreads), 0, stream, cand, row_max,
                      M, V, ws);
+  // sampled path: a histogram of a sixteenth of the candidates picks a bin,
+  // one full pass gathers everything at or above it, and the count decides
+  hipLaunchKernelGGL(topk_sample_hist_kernel, dim3((unsigned)sample_slices(S), (unsigned)B),
+                     dim3(kSliceThreads), 0, stream, cand, M, V, ws);
+  hipLaunchKernelGGL(topk_hist_reduce_kernel, dim3(kHistBins / kReduceBins, (unsigned)B),
+                     dim3(kReduceBins), 0, stream, ws, sample_slices(S), 0);
+  hipLaunchKernelGGL(topk_boundary_kernel<true>, dim3((unsigned)B), dim3(kTopkThreads), 0, stream,
+                     k, ws);
+  hipLaunchKernelGGL(topk_gather_kernel, slices, dim3(kSliceThreads), 0, stream, cand, M, V, ws);
+  hipLaunchKernelGGL(topk_verify_kernel, dim3((unsigned)((B + 63) / 64)), dim3(64), 0, stream, B, k,
+                     ws);
+  // full path, for the requests whose sampled bin did not hold the k best
   hipLaunchKernelGGL(topk_slice_hist_kernel, slices, dim3(kSliceThreads), 0, stream, cand, M, V,
                      ws);
   hipLaunchKernelGGL(topk_hist_reduce_kernel, dim3(kHistBins / kReduceBins, (unsigned)B),
-                     dim3(kReduceBins), 0, stream, ws);
-  hipLaunchKernelGGL(topk_boundary_kernel, dim3((unsigned)B), dim3(kTopkThreads), 0, stream, k,
-                     ws);
+                     dim3(kReduceBins), 0, stream, ws, S, 1);
+  hipLaunchKernelGGL(topk_boundary_kernel<false>, dim3((unsigned)B), dim3(kTopkThreads), 0, stream,
+                     k, ws);
   hipLaunchKernelGGL(topk_gather_kernel, slices, dim3(kSliceThreads), 0, stream, cand, M, V, ws);
   hipLaunchKernelGGL(topk_final_kernel, dim3((unsigned)B), dim3(kTopkThreads), 0, stream, cand, M,
                      V, k, ws, parents, tokens, scores);

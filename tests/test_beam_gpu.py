@@ -91,6 +91,20 @@ def test_beam_topk_row_max_hint_does_not_change_result(gpu, hint):
     _topk_case(gpu, cand, B, M, V, k, row_max=row_max.astype(np.float32))
 
 
+def test_beam_topk_sampled_bin_too_low_falls_back(gpu):
+    """The k best are not spread like the rest: in each request only the first
+    32 candidates (a chunk that the kernel's sixteenth-sample always holds) score
+    high, so the sampled bin has too few candidates above it (32 < k) and the
+    full histogram path must take over.  The result must not change."""
+    B, M, V, k = 2, 64, 512, 64
+    rng = np.random.default_rng(11)
+    cand = (-20.0 - rng.random((B * M, V))).astype(np.float32)
+    for b in range(B):
+        cand[b * M, :32] = (-rng.random(32)).astype(np.float32)
+    _log(f"[beam topk sample miss] B={B} M={M} V={V} k={k}")
+    _topk_case(gpu, cand, B, M, V, k)
+
+
 def test_beam_topk_large_fast_path(gpu):
     """The paper's widths: 1024 beams x 512 tokens per request, k = 1024."""
     B, M, V, k = 8, 1024, 512, 1024
