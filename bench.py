@@ -130,7 +130,8 @@ def cpu_baseline(wl, inp, parents, budget_s=12.0):
 def bench_beam_step(wl, dev, reps=10):
     """Side measurement (not part of `value`): score update + top-k of one step at
     the workload's shape, vocabulary 512, k = M, synthetic bf16 logits and a
-    60 % filter; HIP events on the current stream, medians."""
+    60 % filter, as two calls (candidate array written and read back) and as the
+    fused grace_beam_step; HIP events on the current stream, medians."""
     import torch
     from paper_2608_00938_amd import grace as G
     from paper_2608_00938_amd import workloads as W
@@ -145,8 +146,11 @@ def bench_beam_step(wl, dev, reps=10):
     tok = torch.empty_like(par)
     sc = torch.empty((B, k), dtype=torch.float32, device=dev)
     ws = torch.empty((G.grace_beam_topk_workspace_bytes(B, M, V),), dtype=torch.uint8, device=dev)
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-    ts, tk = [], []
+    ws_step = torch.empty((G.grace_beam_step_workspace_bytes(B, M, V),), dtype=torch.uint8,
+                          device=dev)
+    par2, tok2, sc2 = torch.empty_like(par), torch.empty_like(tok), torch.empty_like(sc)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    ts, tk, tf = [], [], []
     for i in range(reps + 2):
         ev[0].record()
         G.grace_beam_scores(logits, prev, mask, cand=cand, row_max=rmax)
@@ -154,15 +158,23 @@ def bench_beam_step(wl, dev, reps=10):
         G.grace_beam_topk(cand, B, M, k, row_max=rmax, parents=par, tokens=tok, scores=sc,
                           workspace=ws)
         ev[2].record()
+        G.grace_beam_step(logits, prev, B, M, k, mask=mask, parents=par2, tokens=tok2, scores=sc2,
+                          workspace=ws_step)
+        ev[3].record()
         torch.cuda.synchronize()
         if i >= 2:
             ts.append(ev[0].elapsed_time(ev[1]))
             tk.append(ev[1].elapsed_time(ev[2]))
+            tf.append(ev[2].elapsed_time(ev[3]))
     us_s, us_k = float(np.median(ts)) * 1e3, float(np.median(tk)) * 1e3
+    us_f = float(np.median(tf)) * 1e3
+    same = bool(torch.equal(par, par2) and torch.equal(tok, tok2) and
+                torch.equal(sc.view(torch.int32), sc2.view(torch.int32)))
     words = (V + 31) // 32
     bytes_s = R * V * 2 + R * 4 + R * words * 4 + R * V * 4 + R * 4
     return {"shape": f"{B} req x {M} beams x {V} tokens, k={k}", "scores_us": round(us_s, 1),
             "scores_GBs": round(bytes_s / (us_s * 1e-6) / 1e9, 1), "topk_us": round(us_k, 1),
+            "fused_step_us": round(us_f, 1), "fused_step_same_outputs": same,
             "note": "side measurement, not part of value"}
 
 

@@ -287,6 +287,36 @@ int32_t grace_beam_topk(const float* cand, const float* row_max, int32_t B, int3
                         int32_t k, void* workspace, int64_t workspace_bytes, int32_t* parents,
                         int32_t* tokens, float* scores, void* stream);
 
+/* Bytes of device workspace grace_beam_step needs for B, M, V (-1 if out of range). */
+int64_t grace_beam_step_workspace_bytes(int32_t B, int32_t M, int32_t V);
+
+/*
+ * Score update and per-request top-k of one beam step in one call (Sec. 3.1;
+ * dynamic widths, Sec. 3.3): the same parents, tokens and scores, bit for bit,
+ * as grace_beam_scores on these logits, prev_scores and mask (R = B*M rows)
+ * followed by grace_beam_topk on the candidates it writes.  The [R, V]
+ * candidate array is never written: each candidate the selection reads is
+ * recomputed from its logit with the row's log-sum-exp, which a first pass
+ * keeps in the workspace.
+ *
+ *   logits, prev_scores, mask   as for grace_beam_scores, with R = B*M
+ *   B, M, V      requests, beams per request, vocabulary; B*M*V below 2^31
+ *   k            1 <= k <= min(M*V, grace_beam_topk_max_k())
+ *   dtype        GRACE_F32 or GRACE_BF16 (of the logits)
+ *   workspace    device, at least grace_beam_step_workspace_bytes(B, M, V)
+ *                bytes, 8-byte aligned, caller-owned; contents on entry are
+ *                ignored and on return unspecified; calls that share it must
+ *                not overlap
+ *   parents, tokens, scores     as for grace_beam_topk
+ *   stream       hipStream_t
+ * Outputs and the workspace must not overlap each other or the inputs; a
+ * workspace that is too small or misaligned is GRACE_ERR_SHAPE.
+ */
+int32_t grace_beam_step(const void* logits, const float* prev_scores, const uint32_t* mask,
+                        int32_t B, int32_t M, int32_t V, int32_t k, int32_t dtype,
+                        void* workspace, int64_t workspace_bytes, int32_t* parents,
+                        int32_t* tokens, float* scores, void* stream);
+
 /*
  * The CD + GTM index (Sec. 6.4, App. A): the SID trie in CSR form.  Node 0 is
  * the root; node i's child entries are [node_offsets[i], node_offsets[i+1]).

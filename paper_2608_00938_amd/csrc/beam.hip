@@ -51,12 +51,14 @@ __device__ __forceinline__ float load_logit<uint16_t>(const uint16_t* p) {
 
 constexpr int kScoreThreads = 256;
 
-// Generic row kernel (any V): lanes stride over the row.
-template <class T>
+// Generic row kernel (any V): lanes stride over the row.  CAND = false writes
+// only the row's log-sum-exp (lse_out) and best score, for a top-k that
+// recomputes each candidate from the logits.
+template <class T, bool CAND = true>
 __global__ void __launch_bounds__(kScoreThreads)
 beam_scores_kernel(const T* __restrict__ logits, const float* __restrict__ prev,
                    const uint32_t* __restrict__ mask, float* __restrict__ cand,
-                   float* __restrict__ row_max, int32_t R, int32_t V) {
+                   float* __restrict__ row_max, float* __restrict__ lse_out, int32_t R, int32_t V) {
   const int lane = threadIdx.x & 63;
   const int64_t r = (int64_t)blockIdx.x * (kScoreThreads / 64) + (threadIdx.x >> 6);
   if (r >= R) return;   // whole waves
@@ -65,7 +67,7 @@ beam_scores_kernel(const T* __restrict__ logits, const float* __restrict__ prev,
   for (int v = lane; v < V; v += 64) mx = fmaxf(mx, load_logit(x + v));
   mx = wave_max(mx);
   float z = 0.f;
-  for (int v = lane; v < V; v += 64) z += expf(load_logit(x + v) - mx);
+  for (int v = lane; v < V; v += 64) z += fast_exp2((load_logit(x + v) - mx) * kLog2e);
   z = wave_sum(z);
   const float lse = mx + logf(z);
   const float p = prev[r];
@@ -75,75 +77,101 @@ beam_scores_kernel(const T* __restrict__ logits, const float* __restrict__ prev,
   for (int v = lane; v < V; v += 64) {
     const bool ok = mask == nullptr || ((mask[r * words + (v >> 5)] >> (v & 31)) & 1u);
     const float s = ok ? p + (load_logit(x + v) - lse) : -INFINITY;
-    out[v] = s;
+    if constexpr (CAND) out[v] = s;
     best = fmaxf(best, s);
   }
   best = wave_max(best);
   if (row_max != nullptr && lane == 0) row_max[r] = best;
+  if (!CAND && lane == 0) lse_out[r] = lse;
 }
 
+// The row sums of exp take the hardware exp2 of a log2(e)-scaled argument
+// (relative error about 1e-6 per term against 2^-24 for expf), which keeps
+// the pass from being bound by the vector ALU.
 // Row kernel for V a multiple of 8, V <= 512*NCH: each lane owns runs of 8
 // consecutive tokens (one 16-byte bf16 load or two fp32 loads per run), the
 // row stays in registers across the max, sum and output passes.
-template <class T, int NCH>
+template <int NCH>
+constexpr int score_rows_per_wave() { return NCH == 1 ? 4 : (NCH == 2 ? 2 : 1); }
+
+template <class T, int NCH, bool CAND = true>
 __global__ void __launch_bounds__(kScoreThreads)
 beam_scores_vec_kernel(const T* __restrict__ logits, const float* __restrict__ prev,
                        const uint32_t* __restrict__ mask, float* __restrict__ cand,
-                       float* __restrict__ row_max, int32_t R, int32_t V) {
+                       float* __restrict__ row_max, float* __restrict__ lse_out, int32_t R,
+                       int32_t V) {
+  // RPW rows per wave, all their loads issued before the first reduction
+  constexpr int RPW = score_rows_per_wave<NCH>();
   const int lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)blockIdx.x * (kScoreThreads / 64) + (threadIdx.x >> 6);
-  if (r >= R) return;   // whole waves
-  const T* x = logits + r * V;
-  float f[NCH][8];
-  bool live[NCH];
-  float mx = -INFINITY;
-#pragma unroll
-  for (int c = 0; c < NCH; ++c) {
-    const int v0 = c * 512 + 8 * lane;
-    live[c] = v0 < V;
-    if (live[c]) {
-      if constexpr (sizeof(T) == 2) {
-        Chunk<BF16>::unpack(*(const u32x4*)(x + v0), f[c]);
-      } else {
-        Chunk<F32>::unpack(*(const u32x4*)(x + v0), f[c]);
-        Chunk<F32>::unpack(*(const u32x4*)(x + v0 + 4), f[c] + 4);
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) mx = fmaxf(mx, f[c][e]);
-    }
-  }
-  mx = wave_max(mx);
-  float z = 0.f;
-#pragma unroll
-  for (int c = 0; c < NCH; ++c)
-    if (live[c]) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) z += expf(f[c][e] - mx);
-    }
-  z = wave_sum(z);
-  const float lse = mx + logf(z);
-  const float p = prev[r];
+  const int64_t r0 = ((int64_t)blockIdx.x * (kScoreThreads / 64) + (threadIdx.x >> 6)) * RPW;
   const int32_t words = (V + 31) >> 5;
-  float best = -INFINITY;
-  float* out = cand + r * V;
+  float f[RPW][NCH][8];
+  uint32_t bits[RPW][NCH];
+  float p[RPW];
 #pragma unroll
-  for (int c = 0; c < NCH; ++c) {
-    const int v0 = c * 512 + 8 * lane;
-    if (!live[c]) continue;
-    const uint32_t bits = mask == nullptr ? 0xffu : (mask[r * words + (v0 >> 5)] >> (v0 & 31)) & 0xffu;
-    float o[8];
+  for (int j = 0; j < RPW; ++j) {
+    const int64_t r = r0 + j;
+    if (r >= R) continue;   // whole waves
+    const T* x = logits + r * V;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      o[e] = ((bits >> e) & 1u) ? p + (f[c][e] - lse) : -INFINITY;
-      best = fmaxf(best, o[e]);
+    for (int c = 0; c < NCH; ++c) {
+      const int v0 = c * 512 + 8 * lane;
+      if (v0 < V) {
+        if constexpr (sizeof(T) == 2) {
+          Chunk<BF16>::unpack(*(const u32x4*)(x + v0), f[j][c]);
+        } else {
+          Chunk<F32>::unpack(*(const u32x4*)(x + v0), f[j][c]);
+          Chunk<F32>::unpack(*(const u32x4*)(x + v0 + 4), f[j][c] + 4);
+        }
+        bits[j][c] = mask == nullptr ? 0xffu : (mask[r * words + (v0 >> 5)] >> (v0 & 31)) & 0xffu;
+      }
     }
-    // streamed past the caches: the array is larger than L2 and MALL, and
-    // the top-k reads it back with streaming loads as well
-    __builtin_nontemporal_store(Chunk<F32>::pack(o), (u32x4*)(out + v0));
-    __builtin_nontemporal_store(Chunk<F32>::pack(o + 4), (u32x4*)(out + v0 + 4));
+    p[j] = prev[r];
   }
-  best = wave_max(best);
-  if (row_max != nullptr && lane == 0) row_max[r] = best;
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int64_t r = r0 + j;
+    if (r >= R) continue;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+      if (c * 512 + 8 * lane < V) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) mx = fmaxf(mx, f[j][c][e]);
+      }
+    mx = wave_max(mx);
+    float z = 0.f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+      if (c * 512 + 8 * lane < V) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) z += fast_exp2((f[j][c][e] - mx) * kLog2e);
+      }
+    z = wave_sum(z);
+    const float lse = mx + logf(z);
+    float best = -INFINITY;
+    float* out = cand + r * V;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int v0 = c * 512 + 8 * lane;
+      if (v0 >= V) continue;
+      float o[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        o[e] = ((bits[j][c] >> e) & 1u) ? p[j] + (f[j][c][e] - lse) : -INFINITY;
+        best = fmaxf(best, o[e]);
+      }
+      // streamed past the caches: the array is larger than L2 and MALL, and
+      // the top-k reads it back with streaming loads as well
+      if constexpr (CAND) {
+        __builtin_nontemporal_store(Chunk<F32>::pack(o), (u32x4*)(out + v0));
+        __builtin_nontemporal_store(Chunk<F32>::pack(o + 4), (u32x4*)(out + v0 + 4));
+      }
+    }
+    best = wave_max(best);
+    if (row_max != nullptr && lane == 0) row_max[r] = best;
+    if (!CAND && lane == 0) lse_out[r] = lse;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -287,8 +315,74 @@ struct TopkWs {
   }
 };
 
+// Where the top-k reads candidate scores: the array the score kernel wrote,
+// or each score recomputed from the logits with the same operations and the
+// row's stored log-sum-exp, so that both give the same bits.
+struct CandArray {
+  const float* cand;
+  struct Row {   // one request's candidates
+    const float* p;
+    __device__ __forceinline__ float operator[](uint32_t i) const { return p[i]; }
+    __device__ __forceinline__ float nt(uint32_t i) const { return __builtin_nontemporal_load(&p[i]); }
+  };
+  __device__ __forceinline__ Row request(int64_t b, uint32_t N) const {
+    return Row{cand + b * (int64_t)N};
+  }
+};
+
+template <class T>
+struct CandFromLogits {
+  const T* logits;
+  const float* prev;
+  const uint32_t* mask;   // NULL: every token allowed
+  const float* lse;       // per row
+  int32_t M, V;
+  FastDiv per_row;        // request-local candidate index -> beam
+  struct Row {
+    const T* logits;
+    const float* prev;
+    const uint32_t* mask;
+    const float* lse;
+    int64_t r0;
+    int32_t V;
+    FastDiv per_row;
+    __device__ __forceinline__ float operator[](uint32_t i) const {
+      const uint32_t m = per_row.div(i), v = i - m * (uint32_t)V;
+      const int64_t r = r0 + m;
+      const int32_t words = (V + 31) >> 5;
+      const bool ok = mask == nullptr || ((mask[r * words + (v >> 5)] >> (v & 31)) & 1u);
+      return ok ? prev[r] + (load_logit(logits + r * V + v) - lse[r]) : -INFINITY;
+    }
+    __device__ __forceinline__ float nt(uint32_t i) const { return (*this)[i]; }
+    // candidates i .. i+7 (i and V multiples of 8, so one row): one 16-byte
+    // run of logits, as the score kernel's 8-token runs
+    __device__ __forceinline__ void load8(uint32_t i, float (&x)[8]) const {
+      const uint32_t m = per_row.div(i), v = i - m * (uint32_t)V;
+      const int64_t r = r0 + m;
+      const T* row = logits + r * V + v;
+      float f[8];
+      if constexpr (sizeof(T) == 2) {
+        Chunk<BF16>::unpack(*(const u32x4*)row, f);
+      } else {
+        Chunk<F32>::unpack(*(const u32x4*)row, f);
+        Chunk<F32>::unpack(*(const u32x4*)(row + 4), f + 4);
+      }
+      const int32_t words = (V + 31) >> 5;
+      const uint32_t bits =
+          mask == nullptr ? 0xffu : (mask[r * words + (v >> 5)] >> (v & 31)) & 0xffu;
+      const float p = prev[r], l = lse[r];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = ((bits >> e) & 1u) ? p + (f[e] - l) : -INFINITY;
+    }
+  };
+  __device__ __forceinline__ Row request(int64_t b, uint32_t) const {
+    return Row{logits, prev, mask, lse, b * M, V, per_row};
+  }
+};
+
+// Slice s of a request's N candidates; slices start on multiples of 8.
 __device__ __forceinline__ void slice_range(uint32_t N, int S, int s, uint32_t& i0, uint32_t& i1) {
-  const uint32_t per = (N + S - 1) / S;
+  const uint32_t per = ((N + S - 1) / S + 7u) & ~7u;
   i0 = min(N, (uint32_t)s * per);
   i1 = min(N, i0 + per);
 }
@@ -302,8 +396,9 @@ __device__ float block_max_256(float x, float* scratch) {
   return x;
 }
 
+template <class Src>
 __global__ void __launch_bounds__(kSliceThreads)
-topk_slice_max_kernel(const float* __restrict__ cand, const float* __restrict__ row_max,
+topk_slice_max_kernel(Src src, const float* __restrict__ row_max,
                       int32_t M, int32_t V, TopkWs ws) {
   __shared__ float scratch[4];
   const int s = blockIdx.x;
@@ -317,7 +412,7 @@ topk_slice_max_kernel(const float* __restrict__ cand, const float* __restrict__ 
       for (uint32_t m = i0 / V + threadIdx.x; m <= (i1 - 1) / V; m += kSliceThreads)
         best = fmaxf(best, row_max[b * M + m]);
   } else {
-    const float* c = cand + b * (int64_t)N;
+    const auto c = src.request(b, N);
     for (uint32_t i = i0 + threadIdx.x; i < i1; i += kSliceThreads) best = fmaxf(best, c[i]);
   }
   best = block_max_256(best, scratch);
@@ -331,8 +426,11 @@ __device__ __forceinline__ float request_best(const TopkWs& ws, int64_t b) {
   return wave_max(lane < ws.S ? ws.smax[b * ws.S + lane] : -INFINITY);
 }
 
+// VEC8: eight consecutive candidates per thread through Src::Row::load8
+// (V a multiple of 8).
+template <class Src, bool VEC8>
 __global__ void __launch_bounds__(kSliceThreads)
-topk_slice_hist_kernel(const float* __restrict__ cand, int32_t M, int32_t V, TopkWs ws) {
+topk_slice_hist_kernel(Src src, int32_t M, int32_t V, TopkWs ws) {
   __shared__ uint32_t hist[kHistBins];
   const int s = blockIdx.x;
   const int64_t b = blockIdx.y;
@@ -345,7 +443,31 @@ topk_slice_hist_kernel(const float* __restrict__ cand, int32_t M, int32_t V, Top
     const float lo = best - kWindow, inv_w = (float)kHistBins / kWindow;
     uint32_t i0, i1;
     slice_range(N, ws.S, s, i0, i1);
-    const float* c = cand + b * (int64_t)N;
+    const auto c = src.request(b, N);
+    if constexpr (VEC8) {
+      // four runs of eight in flight per thread
+      constexpr uint32_t kBatch = 8 * kSliceThreads;
+      for (uint32_t j0 = i0; j0 < i1; j0 += 4 * kBatch) {
+        float x[4][8];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const uint32_t i = j0 + u * kBatch + 8 * threadIdx.x;
+          if (i < i1) {
+            c.load8(i, x[u]);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) x[u][e] = -INFINITY;
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int bin = window_bin(x[u][e], lo, inv_w);
+            if (bin > 0) atomicAdd(&hist[bin], 1u);
+          }
+      }
+    } else
     // four candidates in flight per thread (streaming loads); one LDS atomic
     // per counted candidate
     for (uint32_t j0 = i0; j0 < i1; j0 += 4 * kSliceThreads) {
@@ -353,7 +475,7 @@ topk_slice_hist_kernel(const float* __restrict__ cand, int32_t M, int32_t V, Top
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const uint32_t i = j0 + u * kSliceThreads + threadIdx.x;
-        x[u] = i < i1 ? __builtin_nontemporal_load(&c[i]) : -INFINITY;
+        x[u] = i < i1 ? c.nt(i) : -INFINITY;
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -382,8 +504,9 @@ __device__ __forceinline__ uint32_t sample_chunk(uint32_t group) {
 constexpr int kSampleGroup = 8;
 __host__ __device__ inline int sample_slices(int S) { return (S + kSampleGroup - 1) / kSampleGroup; }
 
+template <class Src, bool VEC8>
 __global__ void __launch_bounds__(kSliceThreads)
-topk_sample_hist_kernel(const float* __restrict__ cand, int32_t M, int32_t V, TopkWs ws) {
+topk_sample_hist_kernel(Src src, int32_t M, int32_t V, TopkWs ws) {
   __shared__ uint32_t hist[kHistBins];
   const int s = blockIdx.x;
   const int64_t b = blockIdx.y;
@@ -396,7 +519,34 @@ topk_sample_hist_kernel(const float* __restrict__ cand, int32_t M, int32_t V, To
     uint32_t i0, i1, j0, j1;
     slice_range(N, ws.S, s * kSampleGroup, i0, j1);
     slice_range(N, ws.S, min(s * kSampleGroup + kSampleGroup, ws.S) - 1, j0, i1);
-    const float* c = cand + b * (int64_t)N;
+    const auto c = src.request(b, N);
+    if constexpr (VEC8) {
+      // four lanes per sampled chunk (runs of eight), four groups in flight
+      constexpr int kSlots = kSliceThreads / 4;
+      const int q = threadIdx.x >> 2, part = threadIdx.x & 3;
+      const uint32_t g0 = i0 >> 9, g1 = (i1 + 511) >> 9;
+      for (uint32_t gg = g0 + q; gg < g1; gg += 4 * kSlots) {
+        float x[4][8];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const uint32_t g = gg + u * kSlots;
+          const uint32_t i = 32u * sample_chunk(g) + 8 * part;
+          if (g < g1 && i >= i0 && i < i1) {
+            c.load8(i, x[u]);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) x[u][e] = -INFINITY;
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int bin = window_bin(x[u][e], lo, inv_w);
+            if (bin > 0) atomicAdd(&hist[bin], 1u);
+          }
+      }
+    } else {
     // one sampled chunk per 32-lane half-wave and group, eight groups in flight
     const int half = threadIdx.x >> 5, l = threadIdx.x & 31;
     constexpr int kHalves = kSliceThreads / 32;
@@ -407,13 +557,14 @@ topk_sample_hist_kernel(const float* __restrict__ cand, int32_t M, int32_t V, To
       for (int u = 0; u < 8; ++u) {
         const uint32_t g = gg + u * kHalves;
         const uint32_t i = 32u * sample_chunk(g) + l;
-        x[u] = g < g1 && i >= i0 && i < i1 ? __builtin_nontemporal_load(&c[i]) : -INFINITY;
+        x[u] = g < g1 && i >= i0 && i < i1 ? c.nt(i) : -INFINITY;
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int bin = window_bin(x[u], lo, inv_w);
         if (bin > 0) atomicAdd(&hist[bin], 1u);
       }
+    }
     }
   }
   __syncthreads();
@@ -509,9 +660,11 @@ topk_verify_kernel(int32_t B, int32_t k, TopkWs ws) {
 // with one global atomic per flush (same-address global atomics serialise).
 constexpr int kStage = 2048;
 
+template <class Src, bool VEC8>
 __global__ void __launch_bounds__(kSliceThreads)
-topk_gather_kernel(const float* __restrict__ cand, int32_t M, int32_t V, TopkWs ws) {
-  __shared__ uint64_t stage[kStage];
+topk_gather_kernel(Src src, int32_t M, int32_t V, TopkWs ws) {
+  constexpr int kCap = VEC8 ? 2 * kStage : kStage;
+  __shared__ uint64_t stage[kCap];
   __shared__ uint32_t n_stage, base;
   const int s = blockIdx.x;
   const int64_t b = blockIdx.y;
@@ -523,7 +676,7 @@ topk_gather_kernel(const float* __restrict__ cand, int32_t M, int32_t V, TopkWs 
   const float lo = best - kWindow, inv_w = (float)kHistBins / kWindow;
   uint32_t i0, i1;
   slice_range(N, ws.S, s, i0, i1);
-  const float* c = cand + b * (int64_t)N;
+  const auto c = src.request(b, N);
   uint32_t* count = (uint32_t*)&ws.info[b * kInfo + 2];
   uint64_t* list = ws.list + b * (int64_t)kGatherCap;
   if (threadIdx.x == 0) n_stage = 0;
@@ -542,22 +695,56 @@ topk_gather_kernel(const float* __restrict__ cand, int32_t M, int32_t V, TopkWs 
     }
     __syncthreads();
   };
-  for (uint32_t j0 = i0; j0 < i1; j0 += 4 * kSliceThreads) {
-    float x[4];
+  if constexpr (VEC8) {
+    // runs of eight per thread, four batches in flight: each batch is staged
+    // (at most kBatch entries, flushed before the stage can overflow) and the
+    // batch four ahead is loaded in its registers
+    constexpr uint32_t kBatch = 8 * kSliceThreads;
+    float x[4][8];
+    auto load_batch = [&](uint32_t j, float (&y)[8]) __attribute__((always_inline)) {
+      const uint32_t i = j + 8 * threadIdx.x;
+      if (i < i1) {
+        c.load8(i, y);
+      } else {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const uint32_t i = j0 + u * kSliceThreads + threadIdx.x;
-      x[u] = i < i1 ? __builtin_nontemporal_load(&c[i]) : -INFINITY;
-    }
+        for (int e = 0; e < 8; ++e) y[e] = -INFINITY;
+      }
+    };
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const uint32_t i = j0 + u * kSliceThreads + threadIdx.x;
-      const int bin = window_bin(x[u], lo, inv_w);
-      wave_append(stage, &n_stage, i < i1 && bin >= bstar, composite(order_key(x[u]), i), kStage);
+    for (int u = 0; u < 4; ++u) load_batch(i0 + u * kBatch, x[u]);
+    for (uint32_t j0 = i0; j0 < i1; j0 += 4 * kBatch) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t i = j0 + u * kBatch + 8 * threadIdx.x;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int bin = window_bin(x[u][e], lo, inv_w);
+          wave_append(stage, &n_stage, i < i1 && bin >= bstar,
+                      composite(order_key(x[u][e]), i + e), kCap);
+        }
+        __syncthreads();
+        if (n_stage > (uint32_t)(kCap - kBatch)) flush();
+        load_batch(j0 + (u + 4) * kBatch, x[u]);
+      }
     }
-    // at most 4 * kSliceThreads more per iteration: flush before the stage can overflow
-    __syncthreads();
-    if (n_stage > (uint32_t)(kStage - 4 * kSliceThreads)) flush();
+  } else {
+    for (uint32_t j0 = i0; j0 < i1; j0 += 4 * kSliceThreads) {
+      float x[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t i = j0 + u * kSliceThreads + threadIdx.x;
+        x[u] = i < i1 ? c.nt(i) : -INFINITY;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t i = j0 + u * kSliceThreads + threadIdx.x;
+        const int bin = window_bin(x[u], lo, inv_w);
+        wave_append(stage, &n_stage, i < i1 && bin >= bstar, composite(order_key(x[u]), i), kCap);
+      }
+      // at most 4 * kSliceThreads more per iteration: flush before the stage can overflow
+      __syncthreads();
+      if (n_stage > (uint32_t)(kCap - 4 * kSliceThreads)) flush();
+    }
   }
   flush();
 }
@@ -586,15 +773,16 @@ __device__ __forceinline__ float key_score(uint32_t key) {
 
 // Final selection: sort the gathered candidates (fast path), or an exact radix
 // select over all the request's candidates (fallback), then emit k in order.
+template <class Src>
 __global__ void __launch_bounds__(kTopkThreads)
-topk_final_kernel(const float* __restrict__ cand, int32_t M, int32_t V, int32_t k,
+topk_final_kernel(Src src, int32_t M, int32_t V, int32_t k,
                   TopkWs ws, int32_t* __restrict__ parents, int32_t* __restrict__ tokens,
                   float* __restrict__ scores) {
   __shared__ TopkShared sh;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t b = blockIdx.x;
   const uint32_t N = (uint32_t)M * (uint32_t)V;
-  const float* c = cand + b * (int64_t)N;
+  const auto c = src.request(b, N);
   if (tid < 4) sh.ipar[tid] = 0;
 
   uint32_t n_sel;
@@ -763,15 +951,23 @@ topk_final_kernel(const float* __restrict__ cand, int32_t M, int32_t V, int32_t 
   }
 }
 
-hipError_t launch_beam_scores(const void* logits, const float* prev, const uint32_t* mask,
-                              float* cand, float* row_max, int32_t R, int32_t V, bool bf16,
-                              hipStream_t stream) {
+// The score kernels; with CAND = false they write lse_out instead of cand.
+// Both modes pick the same kernel for a given V, so the log-sum-exp (and so
+// every recomputed candidate) matches the written candidates bit for bit.
+template <bool CAND>
+static void launch_scores_mode(const void* logits, const float* prev, const uint32_t* mask,
+                               float* cand, float* row_max, float* lse_out, int32_t R, int32_t V,
+                               bool bf16, hipStream_t stream) {
   const int64_t blocks = ((int64_t)R + kScoreThreads / 64 - 1) / (kScoreThreads / 64);
   const dim3 grid((unsigned)blocks), block(kScoreThreads);
+  constexpr int64_t kWaves = kScoreThreads / 64;
 #define GRACE_SC(TT, NCH)                                                                       \
-  hipLaunchKernelGGL((beam_scores_vec_kernel<TT, NCH>), grid, block, 0, stream,                 \
-                     (const TT*)logits, prev, mask, cand, row_max, R, V)
-  if (V % 8 == 0 && V <= 4096) {
+  hipLaunchKernelGGL((beam_scores_vec_kernel<TT, NCH, CAND>),                                   \
+                     dim3((unsigned)(((int64_t)R + kWaves * score_rows_per_wave<NCH>() - 1) /    \
+                                     (kWaves * score_rows_per_wave<NCH>()))),                    \
+                     block, 0, stream, (const TT*)logits, prev, mask, cand, row_max, lse_out, R, V)
+  // 16-byte runs need V a multiple of 8 and 16-byte aligned logits
+  if (V % 8 == 0 && V <= 4096 && ((uintptr_t)logits & 15) == 0) {
     const int nch = (V + 511) / 512;
     if (bf16) {
       if (nch == 1) GRACE_SC(uint16_t, 1);
@@ -785,13 +981,19 @@ hipError_t launch_beam_scores(const void* logits, const float* prev, const uint3
       else GRACE_SC(float, 8);
     }
   } else if (bf16) {
-    hipLaunchKernelGGL(beam_scores_kernel<uint16_t>, grid, block, 0, stream,
-                       (const uint16_t*)logits, prev, mask, cand, row_max, R, V);
+    hipLaunchKernelGGL((beam_scores_kernel<uint16_t, CAND>), grid, block, 0, stream,
+                       (const uint16_t*)logits, prev, mask, cand, row_max, lse_out, R, V);
   } else {
-    hipLaunchKernelGGL(beam_scores_kernel<float>, grid, block, 0, stream, (const float*)logits,
-                       prev, mask, cand, row_max, R, V);
+    hipLaunchKernelGGL((beam_scores_kernel<float, CAND>), grid, block, 0, stream,
+                       (const float*)logits, prev, mask, cand, row_max, lse_out, R, V);
   }
 #undef GRACE_SC
+}
+
+hipError_t launch_beam_scores(const void* logits, const float* prev, const uint32_t* mask,
+                              float* cand, float* row_max, int32_t R, int32_t V, bool bf16,
+                              hipStream_t stream) {
+  launch_scores_mode<true>(logits, prev, mask, cand, row_max, nullptr, R, V, bf16, stream);
   return hipGetLastError();
 }
 
@@ -799,36 +1001,75 @@ size_t beam_topk_workspace_bytes(int32_t B, int32_t M, int32_t V) {
   return TopkWs::bytes(B, topk_slices((uint32_t)M * (uint32_t)V));
 }
 
-hipError_t launch_beam_topk(const float* cand, const float* row_max, int32_t B, int32_t M,
-                            int32_t V, int32_t k, void* workspace, int32_t* parents,
-                            int32_t* tokens, float* scores, hipStream_t stream) {
+template <class Src, bool VEC8>
+static hipError_t launch_topk_src(Src src, const float* row_max, int32_t B, int32_t M, int32_t V,
+                                  int32_t k, void* workspace, int32_t* parents, int32_t* tokens,
+                                  float* scores, hipStream_t stream) {
   const int S = topk_slices((uint32_t)M * (uint32_t)V);
   const TopkWs ws(workspace, B, S);
   const dim3 slices((unsigned)S, (unsigned)B);
-  hipLaunchKernelGGL(topk_slice_max_kernel, slices, dim3(kSliceThreads), 0, stream, cand, row_max,
+  hipLaunchKernelGGL(topk_slice_max_kernel<Src>, slices, dim3(kSliceThreads), 0, stream, src, row_max,
                      M, V, ws);
   // sampled path: a histogram of a sixteenth of the candidates picks a bin,
   // one full pass gathers everything at or above it, and the count decides
-  hipLaunchKernelGGL(topk_sample_hist_kernel, dim3((unsigned)sample_slices(S), (unsigned)B),
-                     dim3(kSliceThreads), 0, stream, cand, M, V, ws);
+  hipLaunchKernelGGL((topk_sample_hist_kernel<Src, VEC8>), dim3((unsigned)sample_slices(S), (unsigned)B),
+                     dim3(kSliceThreads), 0, stream, src, M, V, ws);
   hipLaunchKernelGGL(topk_hist_reduce_kernel, dim3(kHistBins / kReduceBins, (unsigned)B),
                      dim3(kReduceBins), 0, stream, ws, sample_slices(S), 0);
   hipLaunchKernelGGL(topk_boundary_kernel<true>, dim3((unsigned)B), dim3(kTopkThreads), 0, stream,
                      k, ws);
-  hipLaunchKernelGGL(topk_gather_kernel, slices, dim3(kSliceThreads), 0, stream, cand, M, V, ws);
+  hipLaunchKernelGGL((topk_gather_kernel<Src, VEC8>), slices, dim3(kSliceThreads), 0, stream, src,
+                     M, V, ws);
   hipLaunchKernelGGL(topk_verify_kernel, dim3((unsigned)((B + 63) / 64)), dim3(64), 0, stream, B, k,
                      ws);
   // full path, for the requests whose sampled bin did not hold the k best
-  hipLaunchKernelGGL(topk_slice_hist_kernel, slices, dim3(kSliceThreads), 0, stream, cand, M, V,
-                     ws);
+  hipLaunchKernelGGL((topk_slice_hist_kernel<Src, VEC8>), slices, dim3(kSliceThreads), 0, stream,
+                     src, M, V, ws);
   hipLaunchKernelGGL(topk_hist_reduce_kernel, dim3(kHistBins / kReduceBins, (unsigned)B),
                      dim3(kReduceBins), 0, stream, ws, S, 1);
   hipLaunchKernelGGL(topk_boundary_kernel<false>, dim3((unsigned)B), dim3(kTopkThreads), 0, stream,
                      k, ws);
-  hipLaunchKernelGGL(topk_gather_kernel, slices, dim3(kSliceThreads), 0, stream, cand, M, V, ws);
-  hipLaunchKernelGGL(topk_final_kernel, dim3((unsigned)B), dim3(kTopkThreads), 0, stream, cand, M,
+  hipLaunchKernelGGL((topk_gather_kernel<Src, VEC8>), slices, dim3(kSliceThreads), 0, stream, src,
+                     M, V, ws);
+  hipLaunchKernelGGL(topk_final_kernel<Src>, dim3((unsigned)B), dim3(kTopkThreads), 0, stream, src, M,
                      V, k, ws, parents, tokens, scores);
   return hipGetLastError();
+}
+
+hipError_t launch_beam_topk(const float* cand, const float* row_max, int32_t B, int32_t M,
+                            int32_t V, int32_t k, void* workspace, int32_t* parents,
+                            int32_t* tokens, float* scores, hipStream_t stream) {
+  return launch_topk_src<CandArray, false>(CandArray{cand}, row_max, B, M, V, k, workspace, parents,
+                                           tokens, scores, stream);
+}
+
+size_t beam_step_workspace_bytes(int32_t B, int32_t M, int32_t V) {
+  return beam_topk_workspace_bytes(B, M, V) + (size_t)B * M * 8;
+}
+
+hipError_t launch_beam_step(const void* logits, const float* prev, const uint32_t* mask,
+                            int32_t B, int32_t M, int32_t V, int32_t k, bool bf16, void* workspace,
+                            int32_t* parents, int32_t* tokens, float* scores,
+                            hipStream_t stream) {
+  const int32_t R = B * M;
+  // the top-k workspace, then the rows' log-sum-exp and best scores
+  float* lse = (float*)((char*)workspace + beam_topk_workspace_bytes(B, M, V));
+  float* row_max = lse + R;
+  launch_scores_mode<false>(logits, prev, mask, nullptr, row_max, lse, R, V, bf16, stream);
+  const FastDiv per_row((uint32_t)V);
+#define GRACE_STEP(TT, VEC)                                                                      \
+  return launch_topk_src<CandFromLogits<TT>, VEC>(                                               \
+      CandFromLogits<TT>{(const TT*)logits, prev, mask, lse, M, V, per_row}, row_max, B, M, V, k, \
+      workspace, parents, tokens, scores, stream)
+  // runs of eight: V a multiple of 8 and 16-byte aligned logits
+  const bool vec = V % 8 == 0 && ((uintptr_t)logits & 15) == 0;
+  if (bf16) {
+    if (vec) GRACE_STEP(uint16_t, true);
+    GRACE_STEP(uint16_t, false);
+  }
+  if (vec) GRACE_STEP(float, true);
+  GRACE_STEP(float, false);
+#undef GRACE_STEP
 }
 
 int32_t beam_topk_max_k() { return kGatherCap / 2; }

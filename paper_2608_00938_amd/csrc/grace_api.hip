@@ -268,6 +268,38 @@ int32_t grace_beam_topk(const float* cand, const float* row_max, int32_t B, int3
                                             scores, (hipStream_t)stream));
 }
 
+int64_t grace_beam_step_workspace_bytes(int32_t B, int32_t M, int32_t V) {
+  if (B < 0 || M < 1 || V < 1 || (int64_t)B * M * V >= ((int64_t)1 << 31)) return -1;
+  return (int64_t)grace::beam_step_workspace_bytes(B, M, V);
+}
+
+int32_t grace_beam_step(const void* logits, const float* prev_scores, const uint32_t* mask,
+                        int32_t B, int32_t M, int32_t V, int32_t k, int32_t dtype,
+                        void* workspace, int64_t workspace_bytes, int32_t* parents,
+                        int32_t* tokens, float* scores, void* stream) {
+  if (dtype != GRACE_F32 && dtype != GRACE_BF16) return GRACE_ERR_UNSUPPORTED;
+  if (B < 0 || M < 1 || V < 1 || (int64_t)B * M * V >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
+  if (k < 1 || k > grace::beam_topk_max_k() || (int64_t)k > (int64_t)M * V) return GRACE_ERR_SHAPE;
+  if ((int64_t)B * k >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
+  if (B == 0) return GRACE_OK;
+  if (!logits || !prev_scores || !parents || !tokens || !scores || !workspace) return GRACE_ERR_NULL;
+  const int64_t ws_need = (int64_t)grace::beam_step_workspace_bytes(B, M, V);
+  if (workspace_bytes < ws_need || ((uintptr_t)workspace & 7) != 0) return GRACE_ERR_SHAPE;
+  const int64_t R = (int64_t)B * M, outb = (int64_t)B * k * 4;
+  const Range ins[3] = {{logits, R * V * elem_bytes(dtype)}, {prev_scores, R * 4},
+                        {mask, mask ? R * ((V + 31) / 32) * 4 : 0}};
+  const Range outs[4] = {{parents, outb}, {tokens, outb}, {scores, outb}, {workspace, ws_need}};
+  for (int i = 0; i < 4; ++i) {
+    for (int j = i + 1; j < 4; ++j)
+      if (overlaps(outs[i].p, outs[i].n, outs[j].p, outs[j].n)) return GRACE_ERR_ALIAS;
+    for (const Range& r : ins)
+      if (overlaps(outs[i].p, outs[i].n, r.p, r.n)) return GRACE_ERR_ALIAS;
+  }
+  return hip_status(grace::launch_beam_step(logits, prev_scores, mask, B, M, V, k,
+                                            dtype == GRACE_BF16, workspace, parents, tokens,
+                                            scores, (hipStream_t)stream));
+}
+
 }  // extern "C"
 
 namespace {

@@ -50,6 +50,14 @@ hipError_t launch_beam_topk(const float* cand, const float* row_max, int32_t B, 
 size_t beam_topk_workspace_bytes(int32_t B, int32_t M, int32_t V);
 int32_t beam_topk_max_k();
 
+// Score update and top-k in one: the same outputs as launch_beam_scores then
+// launch_beam_topk, with the candidates recomputed from the logits instead of
+// written out; workspace of beam_step_workspace_bytes(B, M, V) bytes.
+hipError_t launch_beam_step(const void* logits, const float* prev, const uint32_t* mask,
+                            int32_t B, int32_t M, int32_t V, int32_t k, bool bf16, void* workspace,
+                            int32_t* parents, int32_t* tokens, float* scores, hipStream_t stream);
+size_t beam_step_workspace_bytes(int32_t B, int32_t M, int32_t V);
+
 // CD + GTM filter words of every beam row; next trie node of every new beam.
 hipError_t launch_gtm_mask(const grace_gtm_index& index, const grace_gtm_user& user,
                            const int32_t* node_ids, int32_t R, int32_t M, uint32_t* mask,

@@ -64,6 +64,9 @@ _SIGNATURES = {
     "grace_beam_topk_workspace_bytes": [_c_int, _c_int, _c_int],
     "grace_beam_topk": [_c_void_p, _c_void_p, _c_int, _c_int, _c_int, _c_int, _c_void_p,
                         ctypes.c_int64, _c_void_p, _c_void_p, _c_void_p, _c_void_p],
+    "grace_beam_step_workspace_bytes": [_c_int, _c_int, _c_int],
+    "grace_beam_step": [_c_void_p, _c_void_p, _c_void_p, _c_int, _c_int, _c_int, _c_int, _c_int,
+                        _c_void_p, ctypes.c_int64, _c_void_p, _c_void_p, _c_void_p, _c_void_p],
     "grace_gtm_mask": [ctypes.POINTER(GtmIndexC), ctypes.POINTER(GtmUserC), _c_void_p, _c_int,
                        _c_int, _c_void_p, _c_void_p, _c_void_p],
     "grace_trie_advance": [ctypes.POINTER(GtmIndexC), _c_void_p, _c_void_p, _c_void_p, _c_int,
@@ -260,6 +263,38 @@ def grace_beam_topk(cand, B: int, M: int, k: int, row_max=None, parents=None, to
                                    workspace.numel() * workspace.element_size(), _ptr(parents),
                                    _ptr(tokens), _ptr(scores), _stream(cand))
     _check(st, "grace_beam_topk")
+    return parents, tokens, scores
+
+
+def grace_beam_step_workspace_bytes(B: int, M: int, V: int) -> int:
+    return library().grace_beam_step_workspace_bytes(B, M, V)
+
+
+def grace_beam_step(logits, prev_scores, B: int, M: int, k: int, mask=None, parents=None,
+                    tokens=None, scores=None, workspace=None):
+    """Score update and per-request top-k in one call, without the candidate
+    array: the same (parents, tokens, scores) as grace_beam_scores followed by
+    grace_beam_topk.  logits [B*M, V] (fp32 or bf16), prev_scores fp32 [B*M],
+    mask as for grace_beam_scores.  ``workspace``: a device uint8 tensor of at
+    least grace_beam_step_workspace_bytes(B, M, V) bytes (allocated here when
+    not given)."""
+    _contig(logits, prev_scores, mask, parents, tokens, scores, workspace)
+    V = logits.shape[1]
+    dev = logits.device
+    need = grace_beam_step_workspace_bytes(B, M, V)
+    if workspace is None:
+        workspace = torch.empty((max(need, 8),), dtype=torch.uint8, device=dev)
+    if parents is None:
+        parents = torch.empty((B, k), dtype=torch.int32, device=dev)
+    if tokens is None:
+        tokens = torch.empty((B, k), dtype=torch.int32, device=dev)
+    if scores is None:
+        scores = torch.empty((B, k), dtype=torch.float32, device=dev)
+    st = library().grace_beam_step(_ptr(logits), _ptr(prev_scores), _ptr(mask), B, M, V, k,
+                                   _dtype_code(logits), _ptr(workspace),
+                                   workspace.numel() * workspace.element_size(), _ptr(parents),
+                                   _ptr(tokens), _ptr(scores), _stream(logits))
+    _check(st, "grace_beam_step")
     return parents, tokens, scores
 
 

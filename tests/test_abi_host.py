@@ -31,7 +31,8 @@ def test_header_declares_the_boundary():
     for n in ("grace_cross_attn", "grace_kv_append", "grace_self_attn_step",
               "grace_self_attn_step_fused", "grace_self_attn_step_fused_dyn",
               "grace_beam_scores", "grace_beam_topk", "grace_beam_topk_max_k",
-              "grace_beam_topk_workspace_bytes", "grace_gtm_mask", "grace_trie_advance"):
+              "grace_beam_topk_workspace_bytes", "grace_beam_step", "grace_beam_step_workspace_bytes",
+              "grace_gtm_mask", "grace_trie_advance"):
         assert n in names
 
 
@@ -227,6 +228,45 @@ def beam_topk(**kw):
 ])
 def test_beam_topk_rejects(kw, status):
     assert beam_topk(**kw) == status
+
+
+def beam_step(**kw):
+    a = dict(logits=ctypes.c_void_p(0x100000), prev=ctypes.c_void_p(0x180000), mask=None, B=2, M=8,
+             V=64, k=16, dtype=G.GRACE_BF16, ws=ctypes.c_void_p(0x1000000), wsb=1 << 22,
+             par=ctypes.c_void_p(0x200000), tok=ctypes.c_void_p(0x300000),
+             sc=ctypes.c_void_p(0x400000), stream=None)
+    a.update(kw)
+    return G.library().grace_beam_step(a["logits"], a["prev"], a["mask"], a["B"], a["M"], a["V"],
+                                       a["k"], a["dtype"], a["ws"], a["wsb"], a["par"], a["tok"],
+                                       a["sc"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=7), G.GRACE_ERR_UNSUPPORTED),
+    (dict(k=0), G.GRACE_ERR_SHAPE), (dict(k=8 * 64 + 1), G.GRACE_ERR_SHAPE),
+    (dict(B=1 << 10, M=1 << 12, V=1 << 10, k=4), G.GRACE_ERR_SHAPE),   # B*M*V >= 2^31
+    (dict(M=0), G.GRACE_ERR_SHAPE), (dict(M=100, k=5000), G.GRACE_ERR_SHAPE),
+    (dict(logits=None), G.GRACE_ERR_NULL), (dict(prev=None), G.GRACE_ERR_NULL),
+    (dict(sc=None), G.GRACE_ERR_NULL), (dict(ws=None), G.GRACE_ERR_NULL),
+    (dict(wsb=1024), G.GRACE_ERR_SHAPE), (dict(ws=ctypes.c_void_p(0x1000004)), G.GRACE_ERR_SHAPE),
+    (dict(par=ctypes.c_void_p(0x300000 + 8)), G.GRACE_ERR_ALIAS),      # over tokens
+    (dict(sc=ctypes.c_void_p(0x100000 + 40)), G.GRACE_ERR_ALIAS),      # over logits
+    (dict(tok=ctypes.c_void_p(0x180000)), G.GRACE_ERR_ALIAS),          # over prev_scores
+    (dict(mask=ctypes.c_void_p(0x200000 - 64)), G.GRACE_ERR_ALIAS),    # mask over parents
+    (dict(ws=ctypes.c_void_p(0x100000 + 64)), G.GRACE_ERR_ALIAS),      # over logits
+    (dict(B=0), G.GRACE_OK),
+])
+def test_beam_step_rejects(kw, status):
+    assert beam_step(**kw) == status
+
+
+def test_beam_step_workspace_bytes():
+    lib = G.library()
+    assert lib.grace_beam_step_workspace_bytes(2, 0, 64) == -1
+    assert lib.grace_beam_step_workspace_bytes(1 << 10, 1 << 12, 1 << 10) == -1
+    for B, M, V in ((1, 8, 64), (64, 4096, 512)):
+        extra = lib.grace_beam_step_workspace_bytes(B, M, V) - lib.grace_beam_topk_workspace_bytes(B, M, V)
+        assert extra == B * M * 8   # the rows' log-sum-exp and best score
 
 
 def test_beam_topk_max_k_and_workspace():

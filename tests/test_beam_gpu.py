@@ -137,6 +137,41 @@ def test_beam_scores_then_topk_is_a_valid_topk(gpu):
         assert set(clearly.tolist()) <= set(sel.tolist())
 
 
+STEP_CASES = [
+    dict(dtype="bf16", B=3, M=128, V=512, k=300, mask=True),    # 8-token-run score kernel
+    dict(dtype="f32", B=2, M=40, V=100, k=50, mask=True),       # generic score kernel (V % 8 != 0)
+    dict(dtype="bf16", B=2, M=16, V=600, k=4096, mask=False),   # two runs per lane, k = max
+    dict(dtype="bf16", B=2, M=3, V=5, k=15, mask=False),        # k = M*V
+    dict(dtype="bf16", B=8, M=1024, V=512, k=1024, mask=True),  # the paper's widths: sampled path
+    dict(dtype="bf16", B=2, M=32, V=512, k=100, mask=False, equal=True),   # all equal: radix path
+]
+
+
+@pytest.mark.parametrize("i", range(len(STEP_CASES)))
+def test_beam_step_equals_scores_then_topk(gpu, i):
+    """grace_beam_step recomputes each candidate from the logits instead of
+    reading a written array; its outputs must equal grace_beam_scores followed
+    by grace_beam_topk bit for bit."""
+    c = STEP_CASES[i]
+    B, M, V, k = c["B"], c["M"], c["V"], c["k"]
+    R = B * M
+    _log(f"[beam step] {c}")
+    if c.get("equal"):
+        logits = torch.full((R, V), 0.5, device=gpu).to(W.TORCH_DTYPES[c["dtype"]])
+        prev = torch.full((R,), -3.0, device=gpu)
+    else:
+        logits = W.beam_logits(9 + i, 2, R, V, c["dtype"], gpu)
+        prev = torch.from_numpy(W.beam_prev_scores(9 + i, 2, R)).to(gpu)
+    mask = _mask_tensor(W.beam_mask(9 + i, 2, R, V, keep=0.6), gpu) if c["mask"] else None
+    cand, rmax = G.grace_beam_scores(logits, prev, mask)
+    p1, t1, s1 = G.grace_beam_topk(cand, B, M, k, row_max=rmax)
+    p2, t2, s2 = G.grace_beam_step(logits, prev, B, M, k, mask=mask)
+    torch.cuda.synchronize()
+    assert torch.equal(p1, p2), "parents"
+    assert torch.equal(t1, t2), "tokens"
+    assert torch.equal(s1.view(torch.int32), s2.view(torch.int32)), "scores (bitwise)"
+
+
 DYN = [
     dict(dtype="bf16", B=3, H=2, d=64, widths=(1, 5, 12, 12)),
     dict(dtype="f32", B=2, H=3, d=32, widths=(1, 4, 9, 7, 9)),
