@@ -674,6 +674,10 @@ topk_gather_kernel(Src src, int32_t M, int32_t V, TopkWs ws) {
   const uint32_t N = (uint32_t)M * (uint32_t)V;
   const float best = request_best(ws, b);
   const float lo = best - kWindow, inv_w = (float)kHistBins / kWindow;
+  // every candidate in bin b* or above lies at or above the lower edge of bin
+  // b* - 1 (a whole bin of slack against rounding): waves with no candidate
+  // there skip the bin computation
+  const float thr = lo + (float)(bstar - 1) * (kWindow / (float)kHistBins);
   uint32_t i0, i1;
   slice_range(N, ws.S, s, i0, i1);
   const auto c = src.request(b, N);
@@ -718,6 +722,7 @@ topk_gather_kernel(Src src, int32_t M, int32_t V, TopkWs ws) {
         const uint32_t i = j0 + u * kBatch + 8 * threadIdx.x;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
+          if (__ballot(x[u][e] >= thr) == 0) continue;   // whole wave
           const int bin = window_bin(x[u][e], lo, inv_w);
           wave_append(stage, &n_stage, i < i1 && bin >= bstar,
                       composite(order_key(x[u][e]), i + e), kCap);
@@ -737,6 +742,7 @@ topk_gather_kernel(Src src, int32_t M, int32_t V, TopkWs ws) {
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
+        if (__ballot(x[u] >= thr) == 0) continue;   // whole wave
         const uint32_t i = j0 + u * kSliceThreads + threadIdx.x;
         const int bin = window_bin(x[u], lo, inv_w);
         wave_append(stage, &n_stage, i < i1 && bin >= bstar, composite(order_key(x[u]), i), kCap);
