@@ -48,12 +48,10 @@ class DecodeLoop:
         self.x_self = [[torch.empty((B * M, H, d), dtype=dt, device=dev) for M in self.widths]
                        for _ in range(layers)]
         self.prev0 = torch.zeros((B * self.widths[0],), dtype=torch.float32, device=dev)
-        self.cand = [torch.empty((B * M, V), dtype=torch.float32, device=dev) for M in self.widths]
-        self.row_max = [torch.empty((B * M,), dtype=torch.float32, device=dev) for M in self.widths]
         self.parents = [torch.empty((B, k), dtype=torch.int32, device=dev) for k in self.k_out]
         self.tokens = [torch.empty((B, k), dtype=torch.int32, device=dev) for k in self.k_out]
         self.scores = [torch.empty((B, k), dtype=torch.float32, device=dev) for k in self.k_out]
-        ws = max(G.grace_beam_topk_workspace_bytes(B, M, V) for M in self.widths)
+        ws = max(G.grace_beam_step_workspace_bytes(B, M, V) for M in self.widths)
         self.workspace = torch.empty((max(ws, 8),), dtype=torch.uint8, device=dev)
         self.gtm = gtm
         if gtm is not None:
@@ -80,9 +78,8 @@ class DecodeLoop:
                 index, users = self.gtm
                 G.grace_gtm_mask(index, users, self.nodes[t], B, M, mask=self.masks[t],
                                  err_flag=self.gtm_err)
-            G.grace_beam_scores(self.logits[t], prev, self.masks[t], cand=self.cand[t],
-                                row_max=self.row_max[t])
-            G.grace_beam_topk(self.cand[t], B, M, self.k_out[t], row_max=self.row_max[t],
+            # score update + top-k in one call: no [B*M, V] candidate array
+            G.grace_beam_step(self.logits[t], prev, B, M, self.k_out[t], mask=self.masks[t],
                               parents=self.parents[t], tokens=self.tokens[t],
                               scores=self.scores[t], workspace=self.workspace)
             if self.gtm is not None:
