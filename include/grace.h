@@ -21,8 +21,8 @@
  *                         i.e. the parents the rearrangement consumes (Sec. 3.1,
  *                         Sec. 3.3);
  *   grace_gtm_mask        decode-time constraint filter: constrained decoding on
- *                         the SID trie and target matching (Sec. 6, App. A);
- *   grace_trie_advance    the trie node each selected beam moves to (Sec. 6.4);
+ *                         the SID trie and target matching (Sec. 4, Sec. 5.4, App. A);
+ *   grace_trie_advance    the trie node each selected beam moves to (Sec. 4.4);
  *   grace_graph_*         capture of a sequence of these calls (a whole decode
  *                         loop) as one replayable HIP graph (Sec. 5).
  *
@@ -318,7 +318,7 @@ int32_t grace_beam_step(const void* logits, const float* prev_scores, const uint
                         int32_t* tokens, float* scores, void* stream);
 
 /*
- * The CD + GTM index (Sec. 6.4, App. A): the SID trie in CSR form.  Node 0 is
+ * The CD + GTM index (Sec. 4.4, App. A): the SID trie in CSR form.  Node 0 is
  * the root; node i's child entries are [node_offsets[i], node_offsets[i+1]).
  * Entry e leads by token tokens[e] to node child_nodes[e]; its eligibility
  * matchers are row bitmask_index[e] of bitmask_table and row bloom_index[e] of
@@ -345,7 +345,7 @@ typedef struct grace_gtm_index {
 } grace_gtm_index;
 
 /*
- * Request-side targeting attributes (Sec. 6.1, 6.2), one row per request.
+ * Request-side targeting attributes (Sec. 4.2, 4.3), one row per request.
  * Host struct of device pointers.
  */
 typedef struct grace_gtm_user {
@@ -358,7 +358,7 @@ typedef struct grace_gtm_user {
 } grace_gtm_user;
 
 /*
- * Decode-time constraint filter (Sec. 6; lookup of App. A).  Beam row
+ * Decode-time constraint filter (Sec. 4, Sec. 5.4; lookup of App. A).  Beam row
  * r = b*M + m sits at trie node node_ids[r].  Token v is allowed for it when
  *   CD:  some child entry e of the node has tokens[e] = v, and for that entry
  *   GTM: (bitmask_table[bitmask_index[e]] & user.bitmask[b]) == user.bitmask[b]
@@ -383,7 +383,7 @@ int32_t grace_gtm_mask(const grace_gtm_index* index, const grace_gtm_user* user,
                        int32_t* err_flag, void* stream);
 
 /*
- * Trie step after top-k (Sec. 6.4: the selected child node ids become the next
+ * Trie step after top-k (Sec. 4.4: the selected child node ids become the next
  * step's node ids).  New beam i = b*k + j has parent p = parents[i] (request-
  * local, [0, M_prev)) and token tokens[i]:
  *   node_next[i] = child of node_prev[b*M_prev + p] reached by tokens[i],

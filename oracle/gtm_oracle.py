@@ -4,7 +4,7 @@ TEST INFRASTRUCTURE.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
 ``cpu_baseline`` leg of ``bench.py`` may import, call or time this module.  It
 shares no code with the HIP path.
 
-What is computed (GRACE, arXiv 2608.00938, Sec. 6 and App. A):
+What is computed (GRACE, arXiv 2608.00938, Sec. 4, Sec. 5.4 and App. A):
 
 * Constrained decoding.  A beam sits at trie node p (its SID prefix).  Token v
   is admissible only if p||v is a prefix of a valid SID, i.e. v labels one of
@@ -12,9 +12,9 @@ What is computed (GRACE, arXiv 2608.00938, Sec. 6 and App. A):
 * Target matching.  The child entry names a bitmask matcher row and a Bloom
   matcher row (deduplicated tables).  The bitmask test passes when every bit
   of the request's bitmask is present in the node matcher:
-  ``(matcher & user) == user`` over all packed words (Sec. 6.1).  The Bloom
+  ``(matcher & user) == user`` over all packed words (Sec. 4.2).  The Bloom
   test passes when at least one of the request's location filters is
-  contained in the node matcher: ``(loc & matcher) == loc`` (Sec. 6.2).  The
+  contained in the node matcher: ``(loc & matcher) == loc`` (Sec. 4.3).  The
   token survives when both pass.
 * Trie step.  A selected (parent beam, token) moves the new beam to the child
   node reached by that token.
@@ -39,14 +39,14 @@ __all__ = ["bitmask_pass", "bloom_pass", "gtm_mask", "pack_mask", "trie_advance"
 
 
 def bitmask_pass(matcher_words, user_words) -> bool:
-    """Every user attribute bit is present in the node matcher (Sec. 6.1)."""
+    """Every user attribute bit is present in the node matcher (Sec. 4.2)."""
     m = np.asarray(matcher_words, dtype=np.uint64)
     u = np.asarray(user_words, dtype=np.uint64)
     return bool(np.all((m & u) == u))
 
 
 def bloom_pass(matcher_words, user_locations) -> bool:
-    """Some user location's filter is contained in the node matcher (Sec. 6.2)."""
+    """Some user location's filter is contained in the node matcher (Sec. 4.3)."""
     m = np.asarray(matcher_words, dtype=np.uint64)
     for loc in user_locations:
         q = np.asarray(loc, dtype=np.uint64)

@@ -1,4 +1,4 @@
-// Decode-time constraint filter (CD + GTM) and trie step (GRACE, Sec. 6,
+// Decode-time constraint filter (CD + GTM) and trie step (GRACE, Sec. 4, Sec. 5.4,
 // App. A) for gfx950.
 //
 // gtm_mask: 16 lanes per beam row.  The lanes split the beam's child-entry

@@ -4,7 +4,7 @@ Per step t (beam width M_t per request) and decoder layer l:
 cross-attention of the beams over the request's encoder K/V (Sec. 5.1), then
 the fused paged append + self-attention (Sec. 5.2, Sec. 5.3) whose parents are
 the previous step's top-k output.  After the layers, the constraint filter
-(CD + GTM, Sec. 6) of the beams' trie nodes, the beam score update (Sec. 3.1)
+(CD + GTM, Sec. 4, Sec. 5.4) of the beams' trie nodes, the beam score update (Sec. 3.1)
 and top-k with k = M_{t+1} (Sec. 3.3) produce the next step's parents, prefix
 scores and trie nodes on the device, so the whole loop runs without a host
 round trip and is recorded as one graph (Sec. 5).

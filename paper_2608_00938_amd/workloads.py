@@ -268,7 +268,7 @@ def dyn_parents(seed: int, step: int, B: int, M_prev: int, M_cur: int) -> np.nda
 
 
 # ---------------------------------------------------------------------------
-# Synthetic CD+GTM index (Sec. 6, App. A) and request attributes.  The paper's
+# Synthetic CD+GTM index (Sec. 4, App. A) and request attributes.  The paper's
 # 30M-SID index and its targeting data are not public; this builds an index of
 # the same form: a SID trie in CSR form whose child entries point to
 # deduplicated bitmask (W_bm = 7 words) and Bloom (W_bl = 4 words) matcher rows,

@@ -1,7 +1,7 @@
 """Parity of the CD+GTM constraint filter and the trie step with the oracle,
 through the C ABI on the GPU.  Both are integer/bit work: compared bit-exactly.
 The index is synthetic (the paper's 30M-SID index and targeting data are not
-public); its form follows Sec. 6.4 and App. A."""
+public); its form follows Sec. 4.4 and App. A."""
 import sys
 
 import numpy as np

@@ -4,7 +4,7 @@ Independent of the oracle's code path: the paper's printed toy example
 (``tests/golden/gtm_toy_bitmask.txt``), closed Bloom-containment cases, a trie
 rebuilt from the SID list with Python sets, ad-level brute force (the node test
 must never reject a child that holds an eligible ad: the union test is
-conservative, Sec. 6.1-6.2), and exactness where a node holds a single ad.
+conservative, Sec. 4.2-4.3), and exactness where a node holds a single ad.
 """
 import os
 
@@ -132,7 +132,7 @@ def _ad_eligible(index, users, b, ads):
 
 
 def test_union_test_is_conservative_and_exact_for_single_ads(small):
-    """No child holding an eligible ad is filtered (Sec. 6.1-6.2); where the child
+    """No child holding an eligible ad is filtered (Sec. 4.2-4.3); where the child
     subtree holds exactly one ad, the node test is the ad test."""
     index, users = small
     pre = _node_prefixes(index)
