@@ -9,9 +9,9 @@
 // bf16 path (MFMA, cross_attn_bf16_kernel).  Each wave owns 64 beams (32 at
 // head dim 128) and computes, per 32-key step,
 //   S^T = K Q^T           v_mfma_f32_32x32x16_bf16; A = K rows from LDS, B = Q^T
-//                         (pre-multiplied by scale*log2(e)) held in registers,
-//                         so S^T holds exp2 arguments;
-//   P = exp2(S^T)         VALU, packed to bf16 in place;
+//                         (the input bf16 values) held in registers;
+//   P = exp2(c S^T)       VALU, c = scale*log2(e) applied to the fp32 scores,
+//                         packed to bf16 in place;
 //   O^T += V^T P^T        A = V^T read with ds_read_b64_tr_b16, B = P^T taken
 //                         straight from the S^T registers;
 //   l += 1^T P^T          the row sums of the applied bf16 weights, on the
@@ -157,17 +157,6 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
-__device__ __forceinline__ float round_to_bf16(float x) {
-  return __uint_as_float((pack_bf16x2(x, 0.f) & 0xffffu) << 16);
-}
-
-// x rounded to the nearest value that is the sum of two bf16 numbers hi + lo
-// with hi = bf16(x) (16 significant bits).
-__device__ __forceinline__ float round_to_bf16x2(float x) {
-  const float h = round_to_bf16(x);
-  return h + round_to_bf16(x - h);
-}
-
 // max(a, b, c) as one v_max3_f32.  Written as asm: built from fmaxf the
 // compiler first canonicalises every MFMA result (one extra v_max per value).
 __device__ __forceinline__ float max3(float a, float b, float c) {
@@ -202,8 +191,10 @@ __device__ __forceinline__ float max_with_other_half(float x) {
 //
 // in a fixed issue order: every 32x32x16 product is followed by the VALU work
 // that fits under it (two exp2 at the quarter rate), so that one wave alone
-// keeps both the matrix core and the VALU busy.  Q^T (times scale*log2 e,
-// re-rounded to bf16) stays in registers.
+// keeps both the matrix core and the VALU busy.  Q^T stays in registers as
+// the input bf16 values; the softmax scale (times log2 e) multiplies the fp32
+// scores just before exp2, so the only roundings ahead of the softmax are those
+// of the inputs themselves.
 //
 // Stream.  K and V pass through two four-buffer LDS rings in tiles of kTileN
 // keys, K one tile ahead of V: at the start of tile T the workgroup issues
@@ -218,8 +209,8 @@ __device__ __forceinline__ float max_with_other_half(float x) {
 // pipelined): an exponent shift per beam that starts at 0 and moves only when
 // the first step's maximum lies outside [-64, 32] or a later step's maximum
 // exceeds the shift by more than 32.  Then the shift becomes the running
-// maximum (a bf16 hi+lo pair, 16 significant bits), O and the row sums are
-// rescaled, and a rank-1 MFMA term subtracts the shift inside the S^T product.
+// maximum, O and the row sums are rescaled, and every later score enters exp2
+// as fma(S, c, -shift) in fp32.
 // With the shift bounded this way exp2 never overflows (P <= 2^32) and the
 // largest weight of a beam is at least 2^-64, so the safe pass gives the
 // softmax of the definition for any input; the fast pass is kept only when its
@@ -408,11 +399,7 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
 #pragma unroll
       for (int ks = 0; ks < C::kKS; ++ks) {
         const u32x4 u = *(const u32x4*)(qbuf + C::slot(mb * 32 + l32, 2 * ks + hi) * 16);
-        float f[8];
-        Chunk<BF16>::unpack(u, f);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) f[e] *= c;
-        qf[mb][ks] = __builtin_bit_cast(bf16x8, Chunk<BF16>::pack(f));
+        qf[mb][ks] = __builtin_bit_cast(bf16x8, u);
       }
   } else {
 #pragma unroll
@@ -469,8 +456,7 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
 
   f32x16 o[C::kDB][C::kMB];
   f32x4 lsum = {0.f, 0.f, 0.f, 0.f};   // lanes 0-15: rows 2mb / 2mb+1 = beams c / c+16 of block mb
-  float shift[C::kMB];
-  bool biased = false;
+  float shift[C::kMB];   // safe pass: exponent shift of this lane's beam, exp2 units
   auto reset_acc = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int mb = 0; mb < C::kMB; ++mb) {
@@ -481,7 +467,6 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
         for (int r = 0; r < 16; ++r) o[db][mb][r] = 0.f;
     }
     lsum = f32x4{0.f, 0.f, 0.f, 0.f};
-    biased = false;
   };
   reset_acc();
 
@@ -608,7 +593,7 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
           for (int c2 = 0; c2 < count; ++c2) {
             const int it = next_item + c2;
             if (it < 8) {
-              s[r0 + it] = fast_exp2(s[r0 + it]);
+              s[r0 + it] = fast_exp2(s[r0 + it] * c);
             } else if (it < 12) {
               const int w = it - 8;
               pw[w] = pack_bf16x2(s[r0 + 2 * w], s[r0 + 2 * w + 1]);
@@ -736,23 +721,14 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
       const int issued = prefetch(T);
       const int buf = T & (C::kNBuf - 1);
       if (active) {
+#pragma unroll 1
         for (int s = 0; s < C::kSub; ++s) {
           const int32_t j = T * C::kSub + s;
           if (j >= n_sub) break;
-          // S(j)^T, minus the shift as a rank-1 term when any beam has one
+          // S(j)^T, then the exp2 arguments c*S - shift in fp32
           f32x16 sc[C::kMB];
 #pragma unroll
-          for (int mb = 0; mb < C::kMB; ++mb) {
-            sc[mb] = zero16;
-            if (biased) {
-              const float nhi = round_to_bf16(-shift[mb]);
-              const uint32_t nb = pack_bf16x2(nhi, -shift[mb] - nhi);
-              const bf16x8 one_a =
-                  __builtin_bit_cast(bf16x8, u32x4{hi == 0 ? 0x3f803f80u : 0u, 0u, 0u, 0u});
-              const bf16x8 bias_b = __builtin_bit_cast(bf16x8, u32x4{hi == 0 ? nb : 0u, 0u, 0u, 0u});
-              sc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(one_a, bias_b, zero16, 0, 0, 0);
-            }
-          }
+          for (int mb = 0; mb < C::kMB; ++mb) sc[mb] = zero16;
 #pragma unroll
           for (int ks = 0; ks < C::kKS; ++ks) {
             const bf16x8 kf = read_k(buf, s, ks);
@@ -760,6 +736,10 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
             for (int mb = 0; mb < C::kMB; ++mb)
               sc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[mb][ks], sc[mb], 0, 0, 0);
           }
+#pragma unroll
+          for (int mb = 0; mb < C::kMB; ++mb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) sc[mb][r] = __builtin_fmaf(sc[mb][r], c, -shift[mb]);
           mask_step(sc, j);
           // each beam's maximum; move the shift of beams that need it
           float mx[C::kMB];
@@ -778,7 +758,7 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
             for (int mb = 0; mb < C::kMB; ++mb) {
               const bool need =
                   j == 0 ? (mx[mb] > C::kShiftHi || mx[mb] < C::kShiftLo) : mx[mb] > C::kShiftHi;
-              const float ns = need ? round_to_bf16x2(shift[mb] + mx[mb]) : shift[mb];
+              const float ns = need ? shift[mb] + mx[mb] : shift[mb];
               const float delta = ns - shift[mb];
               alpha[mb] = fast_exp2(-delta);
               shift[mb] = ns;
@@ -793,7 +773,6 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
 #pragma unroll
                 for (int r = 0; r < 16; ++r) o[db][mb][r] *= alpha[mb];
             }
-            biased = true;
           }
 #pragma unroll
           for (int kc = 0; kc < 2; ++kc) {

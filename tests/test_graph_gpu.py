@@ -1,10 +1,15 @@
 """A whole decode loop (layers x steps of cross-attention and fused paged
 self-attention, then score update and top-k feeding the next step's parents)
-recorded as one HIP graph replays bit-identically to the same loop run eagerly.
+recorded as one HIP graph.
 
 The graph is replayed several times with eager library work, host
 synchronisations and overwritten outputs in between; every replay must
-reproduce every output of the eager run exactly.
+reproduce every output of the eager run exactly.  After a replay, every output
+of every layer and step is also checked against the oracle, fed with the
+parents the loop itself chose on the GPU: attention outputs within 2e-2, block
+tables (the last two steps': the two tables alternate), filter words and trie
+nodes bit-exact, and each step's selection a
+valid top-k of the fp64 candidate scores (scores within 1e-4).
 """
 import math
 import sys
@@ -14,6 +19,8 @@ import pytest
 import torch
 
 import oracle
+from oracle import beam_oracle as BO
+from oracle import gtm_oracle as GO
 from paper_2608_00938_amd import decode as D
 from paper_2608_00938_amd import grace as G
 from paper_2608_00938_amd import workloads as W
@@ -50,7 +57,11 @@ def _make_loop(dev, B=2, widths=(1, 8, 16, 16), H=2, d=64, V=64, layers=2, L=24,
 
 def _gtm(dev, B, seed=41):
     ix = W.gtm_index(seed, 20000)
-    return ix, (G.GtmIndex(ix, dev), G.GtmUsers(W.gtm_users(seed, B, L_max=16), dev))
+    return ix, (G.GtmIndex(ix, dev), G.GtmUsers(_users(B, seed), dev))
+
+
+def _users(B, seed=41):
+    return W.gtm_users(seed, B, L_max=16)
 
 
 def _snapshot(loop):
@@ -170,3 +181,102 @@ def test_decode_loop_with_filter_follows_the_trie(gpu):
                 assert hit, (b, j, seq)
                 node = int(child[hit[0]])
             assert node == node_last[b, j]
+
+
+def _f64(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def _check_topk(cand, par, tok, sc, B, M, V, k, eps=1e-4):
+    """The GPU's selection is a top-k of the fp64 candidates up to the scores'
+    error: k distinct candidates, each within eps of the k-th best score or
+    above it, every candidate clearly above the k-th taken, the reported
+    scores those of the selected candidates (-inf exactly), best first."""
+    for b in range(B):
+        s = cand[b * M:(b + 1) * M].reshape(-1)
+        kth = np.sort(s)[::-1][k - 1]
+        sel = par[b].astype(np.int64) * V + tok[b]
+        assert np.all((par[b] >= 0) & (par[b] < M)) and np.all((tok[b] >= 0) & (tok[b] < V))
+        assert len(set(sel.tolist())) == k
+        assert np.all(s[sel] >= kth - eps)
+        clearly = np.nonzero(s > kth + eps)[0]
+        assert set(clearly.tolist()) <= set(sel.tolist())
+        ref = s[sel]
+        fin = np.isfinite(ref)
+        assert np.array_equal(np.isneginf(sc[b]), np.isneginf(ref))
+        assert np.all(np.abs(sc[b][fin] - ref[fin]) <= eps)
+        assert np.all(np.diff(sc[b][fin]) <= 0) and np.all(fin[:fin.sum()])
+
+
+@pytest.mark.parametrize("with_gtm", [False, True], ids=["given_masks", "cd_gtm"])
+def test_decode_loop_matches_oracle(gpu, with_gtm):
+    """The replayed loop at widths (1, 8, 16, 16), two layers, against the
+    oracle at every layer and step."""
+    B = 2
+    ix = us = None
+    gtm = None
+    if with_gtm:
+        ix, gtm = _gtm(gpu, B)
+        us = _users(B)
+    loop, inp = _make_loop(gpu, V=512 if with_gtm else 64, gtm=gtm)
+    stream = torch.cuda.Stream()
+    graph = loop.capture(stream)
+    graph.launch(stream)
+    stream.synchronize()
+    graph.destroy()
+    _log(f"[graph oracle] widths {loop.widths} layers {loop.layers} gtm={with_gtm}")
+    B, V, H, d, T = loop.B, loop.V, loop.H, loop.d, loop.T
+    R_s = B * max(loop.widths)
+    scale = 1.0 / math.sqrt(d)
+    ek, ev = _f64(loop.enc_k), _f64(loop.enc_v)
+    par = [p.cpu().numpy() for p in loop.parents]
+    tok = [x.cpu().numpy() for x in loop.tokens]
+    sc = [x.cpu().numpy().astype(np.float64) for x in loop.scores]
+    tables = [None] * loop.layers
+    pools = [(np.zeros((T, R_s, H, d)), np.zeros((T, R_s, H, d))) for _ in range(loop.layers)]
+    worst_c = worst_s = 0.0
+    for t, M in enumerate(loop.widths):
+        M_prev = loop.widths[t - 1] if t > 0 else 1
+        R = B * M
+        par_t = par[t - 1].reshape(-1) if t > 0 else None
+        for l in range(loop.layers):
+            x = loop.inputs[l][t]
+            ref = oracle.cross_attn(_f64(x["q_cross"]), ek, ev, inp.offsets, M, scale)
+            err = float(np.max(np.abs(_f64(loop.x_cross[l][t]) - ref)))
+            assert err <= 2e-2, (l, t, "cross", err)
+            worst_c = max(worst_c, err)
+            tnew = BO.kv_append_table_dyn(tables[l], par_t, B, M_prev, M, t, R_s)
+            if t >= T - 2:   # the two tables alternate: the last two steps' survive the loop
+                got = loop.caches[l].table(t)[:R, :t + 1].cpu().numpy()
+                assert np.array_equal(got, tnew), (l, t, "table")
+            full = np.zeros((R, T), dtype=np.int64)
+            full[:, :t + 1] = tnew
+            tables[l] = full
+            kp, vp = pools[l]
+            kp[t, :R] = _f64(x["k_new"])
+            vp[t, :R] = _f64(x["v_new"])
+            ref = oracle.self_attn_step(_f64(x["q_self"]), kp, vp, full, t, scale)
+            err = float(np.max(np.abs(_f64(loop.x_self[l][t]) - ref)))
+            assert err <= 2e-2, (l, t, "self", err)
+            worst_s = max(worst_s, err)
+        # the filter of this step's beams
+        if with_gtm:
+            nodes = loop.nodes[t].cpu().numpy()
+            allowed = GO.gtm_mask(ix, us, nodes, B, M)
+            words = loop.masks[t].cpu().numpy().view(np.uint32)
+            assert np.array_equal(words, GO.pack_mask(allowed)), (t, "mask")
+        else:
+            allowed = BO.unpack_mask(loop.masks[t].cpu().numpy().view(np.uint32), V)
+        prev = np.zeros(R) if t == 0 else sc[t - 1].reshape(-1)
+        cand = BO.candidate_scores(_f64(loop.logits[t]), prev, allowed)
+        _check_topk(cand, par[t], tok[t], sc[t], B, M, V, loop.k_out[t])
+        if with_gtm:
+            nxt = GO.trie_advance(ix, loop.nodes[t].cpu().numpy(), par[t].reshape(-1),
+                                  tok[t].reshape(-1), B, M, loop.k_out[t])
+            assert np.array_equal(loop.nodes[t + 1].cpu().numpy(), nxt), (t, "trie")
+        _log(f"  step {t} (M {M_prev}->{M}): attention, tables, filter and top-k match")
+    _log(f"  worst cross err {worst_c:.3e}, worst self err {worst_s:.3e}")
+    for c in loop.caches:
+        assert int(c.err_flag.item()) == 0
+    if with_gtm:
+        assert int(loop.gtm_err.item()) == 0

@@ -1,13 +1,19 @@
 """Parity of the HIP path (through the C ABI) with the fp64 oracle on the GPU.
 
-Small workloads are compared element by element on every output; the two
-largest are compared on sampled rows the oracle computes one request / one
-ancestor chain at a time, in exactly the launch configuration the benchmark
-times.  Tolerances: max abs error <= 2e-2 for bf16 inputs (fp32 accumulation),
-<= 1e-5 for fp32.  Integer work (block tables) and the pool copy are bit-exact.
+Every workload is compared element by element.  On the two largest (64 x 4096
+beams and the ragged 128 x 2048), in exactly the launch configuration the
+benchmark times, every self-attention output and block-table entry of every
+step is checked, and every cross-attention output of the first and the last
+step; the oracle then runs request by request in a pool of host threads, and
+the steps in between are checked on sampled rows.  Tolerances: max abs error
+<= 2e-2 for bf16 inputs (fp32 accumulation), <= 1e-5 for fp32.  Integer work
+(block tables) and the pool copy are bit-exact.  Outputs start as NaN, so a
+row the kernels never write cannot pass.
 """
 import math
+import os
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 import pytest
@@ -52,12 +58,13 @@ class Decode:
         kn = inp.step_tensor("k_new", t)
         vn = inp.step_tensor("v_new", t)
         par = None if self.parents[t] is None else torch.from_numpy(self.parents[t]).to(qc.device)
-        xc = G.grace_cross_attn(qc, self.enc_k, self.enc_v, self.off, wl.M, self.scale)
+        nan = lambda: torch.full_like(qc, float("nan"))  # noqa: E731
+        xc = G.grace_cross_attn(qc, self.enc_k, self.enc_v, self.off, wl.M, self.scale, out=nan())
         if self.fused:
-            xs = self.cache.append_attend(t, qs, kn, vn, par, self.scale)
+            xs = self.cache.append_attend(t, qs, kn, vn, par, self.scale, out=nan())
         else:
             self.cache.append(t, kn, vn, par)
-            xs = self.cache.attend(t, qs, self.scale)
+            xs = self.cache.attend(t, qs, self.scale, out=nan())
         rec = dict(qc=qc, qs=qs, kn=kn, vn=vn, xc=xc, xs=xs,
                    table=self.cache.table(t).clone())
         self.steps.append(rec)
@@ -104,23 +111,25 @@ def _sample_rows(wl, rng, n=48):
     return np.array(sorted(set(rows)), dtype=np.int64)
 
 
-def _sampled_check(dec, rng):
-    """Sampled rows, each computed by the oracle from its request / ancestor chain."""
+def _sampled_check(dec, rng, cross_steps=None):
+    """Sampled rows, each computed by the oracle from its request / ancestor
+    chain (cross-attention only at ``cross_steps``, default every step)."""
     wl = dec.wl
     rows = _sample_rows(wl, rng)
     dev = dec.enc_k.device
     idx = torch.from_numpy(rows).to(dev)
     for t, rec in enumerate(dec.steps):
-        # cross-attention: one request at a time
-        got = _np(rec["xc"].index_select(0, idx))
-        ref = np.empty_like(got)
-        for b in np.unique(rows // wl.M):
-            sel = np.nonzero(rows // wl.M == b)[0]
-            o0, o1 = int(dec.inp.offsets[b]), int(dec.inp.offsets[b + 1])
-            ref[sel] = oracle.cross_attn_request(_np(rec["qc"].index_select(0, idx[sel])),
-                                                 _np(dec.enc_k[o0:o1]), _np(dec.enc_v[o0:o1]),
-                                                 dec.scale)
-        _check_close(got, ref, wl.dtype, f"cross t={t} ({len(rows)} sampled rows)")
+        if cross_steps is None or t in cross_steps:
+            # cross-attention: one request at a time
+            got = _np(rec["xc"].index_select(0, idx))
+            ref = np.empty_like(got)
+            for b in np.unique(rows // wl.M):
+                sel = np.nonzero(rows // wl.M == b)[0]
+                o0, o1 = int(dec.inp.offsets[b]), int(dec.inp.offsets[b + 1])
+                ref[sel] = oracle.cross_attn_request(_np(rec["qc"].index_select(0, idx[sel])),
+                                                     _np(dec.enc_k[o0:o1]), _np(dec.enc_v[o0:o1]),
+                                                     dec.scale)
+            _check_close(got, ref, wl.dtype, f"cross t={t} ({len(rows)} sampled rows)")
         # block table rows from the parents alone, bit-exact
         tab = oracle.table_rows(rows, t, dec.parents, wl.B, wl.M)
         gpu_tab = rec["table"].index_select(0, idx).cpu().numpy()[:, :t + 1]
@@ -150,20 +159,103 @@ def test_workload_full_parity(gpu, name, fused):
     _full_check(dec)
 
 
+def _pool():
+    """Host threads for the oracle (numpy releases the GIL in its matrix products
+    and ufuncs), one BLAS thread each."""
+    return ThreadPoolExecutor(max_workers=max(1, min(16, os.cpu_count() or 1)))
+
+
+def _blas_single_thread():
+    from threadpoolctl import threadpool_limits
+    return threadpool_limits(limits=1)
+
+
+def _cross_full_check(dec, t, chunk=1024):
+    """Every cross-attention row of step t against the oracle, one (request,
+    beam chunk) per oracle call."""
+    wl = dec.wl
+    qh = dec.steps[t]["qc"].float().cpu().numpy()
+    got = dec.steps[t]["xc"].float().cpu().numpy()
+    ek, ev = dec.enc_k.float().cpu().numpy(), dec.enc_v.float().cpu().numpy()
+    off = dec.inp.offsets
+
+    def one(b, m0):
+        rows = slice(b * wl.M + m0, b * wl.M + min(wl.M, m0 + chunk))
+        ref = oracle.cross_attn_request(qh[rows], ek[off[b]:off[b + 1]], ev[off[b]:off[b + 1]],
+                                        dec.scale)
+        g = got[rows].astype(np.float64)
+        return (float(np.max(np.abs(g - ref))), bool(np.all(np.isfinite(g))),
+                float(np.max(np.abs(ref))))
+
+    with _blas_single_thread(), _pool() as ex:
+        res = list(ex.map(lambda a: one(*a), [(b, m0) for b in range(wl.B)
+                                              for m0 in range(0, wl.M, chunk)]))
+    err = max(r[0] for r in res)
+    _log(f"  cross t={t} all {wl.R} rows: max|err| = {err:.3e}  max|out| = "
+         f"{max(r[2] for r in res):.3f}")
+    assert all(r[1] for r in res), f"cross t={t}: non-finite output"
+    assert err <= TOL[wl.dtype], f"cross t={t}: {err} > {TOL[wl.dtype]}"
+
+
+def _self_full_check(dec, chunk=32768):
+    """Every block-table entry (bit-exact) and every self-attention row of every
+    step against the oracle: the table from the oracle's update rule over the
+    whole batch, each row's prefix gathered from the step inputs through it."""
+    wl = dec.wl
+    dev = dec.enc_k.device
+    table = None
+    for t, rec in enumerate(dec.steps):
+        table = oracle.kv_append_table(table, dec.parents[t], wl.B, wl.M, t)
+        gpu_table = rec["table"].cpu().numpy()[:, :t + 1]
+        assert np.array_equal(gpu_table, table), f"table t={t}"
+        # each prefix position's rows, by slab: block id j*R + r is row r of step j
+        src = [torch.from_numpy(np.ascontiguousarray(table[:, j] - j * wl.R)).to(dev)
+               for j in range(t + 1)]
+        jobs = []
+        with _blas_single_thread(), _pool() as ex:
+            for r0 in range(0, wl.R, chunk):
+                sl = slice(r0, min(wl.R, r0 + chunk))
+                q = rec["qs"][sl].float().cpu().numpy()
+                kpre = np.stack([dec.steps[j]["kn"].index_select(0, src[j][sl]).float().cpu().numpy()
+                                 for j in range(t + 1)], axis=1)
+                vpre = np.stack([dec.steps[j]["vn"].index_select(0, src[j][sl]).float().cpu().numpy()
+                                 for j in range(t + 1)], axis=1)
+                g = rec["xs"][sl].float().cpu().numpy()
+
+                def one(q=q, kpre=kpre, vpre=vpre, g=g):
+                    ref = oracle.self_attn_rows(q, kpre, vpre, dec.scale)
+                    g = g.astype(np.float64)
+                    return (float(np.max(np.abs(g - ref))), bool(np.all(np.isfinite(g))),
+                            float(np.max(np.abs(ref))))
+                jobs.append(ex.submit(one))
+            res = [j.result() for j in jobs]
+        err = max(r[0] for r in res)
+        _log(f"  self t={t} all {wl.R} rows: max|err| = {err:.3e}  max|out| = "
+             f"{max(r[2] for r in res):.3f}")
+        assert all(r[1] for r in res), f"self t={t}: non-finite output"
+        assert err <= TOL[wl.dtype], f"self t={t}: {err} > {TOL[wl.dtype]}"
+        assert torch.equal(dec.cache.k_pool[t], rec["kn"]) and torch.equal(dec.cache.v_pool[t], rec["vn"])
+
+
 @pytest.mark.parametrize("fused", [False, True], ids=["split", "fused"])
 @pytest.mark.parametrize("name", ["bf16_b64_m4096", "bf16_ragged_b128_m2048"])
-def test_workload_sampled_parity(gpu, name, fused):
+def test_large_workload_parity(gpu, name, fused):
+    """Full size, the benchmark's launch configuration.  Self-attention and the
+    tables: every row of every step.  Cross-attention (the same kernel on both
+    self-attention paths): every row of step 0 on the split run and of the last
+    step on the fused run; the other steps on sampled rows."""
     wl = W.WORKLOADS[name]
-    _log(f"[parity sampled] {name} seed=0 fused={fused}")
+    _log(f"[parity large] {name} seed=0 fused={fused}")
     dec = Decode(wl, 0, gpu, fused)
     for t in range(wl.steps):
         dec.run_step(t)
     torch.cuda.synchronize()
     assert int(dec.cache.err_flag.item()) == 0
-    _sampled_check(dec, np.random.default_rng(0))
-    # properties at full size: finite everywhere; t=0 self-attention is v_new
-    for rec in dec.steps:
-        assert bool(torch.isfinite(rec["xc"]).all()) and bool(torch.isfinite(rec["xs"]).all())
+    _self_full_check(dec)
+    t_full = wl.steps - 1 if fused else 0
+    _cross_full_check(dec, t_full)
+    _sampled_check(dec, np.random.default_rng(0), cross_steps=[t for t in range(wl.steps)
+                                                               if t != t_full])
     assert torch.equal(dec.steps[0]["xs"], dec.steps[0]["vn"])
 
 
@@ -426,9 +518,7 @@ def _extreme_case(gpu, kind, B=3, M=96, H=2, d=64, L=200, seed=13):
 @pytest.mark.parametrize("kind", ["huge", "tiny"])
 def test_cross_attn_extreme_scores_take_the_safe_pass(gpu, kind):
     """Scores whose exp2 sums leave [2^-100, 2^64] fail the fast pass's check;
-    the workgroup's safe pass (exponent shift) still matches the fp64 oracle.
-    (The inputs are well conditioned: with many near-tied scores of this size,
-    the bf16 rounding of the pre-scaled queries alone moves the weights.)"""
+    the workgroup's safe pass (exponent shift) still matches the fp64 oracle."""
     q, k, v, off = _extreme_case(gpu, kind)
     M = q.shape[0] // (off.numel() - 1)
     _log(f"[cross extreme] {kind}")
@@ -436,3 +526,65 @@ def test_cross_attn_extreme_scores_take_the_safe_pass(gpu, kind):
     torch.cuda.synchronize()
     ref = oracle.cross_attn(_np(q), _np(k), _np(v), off.numpy(), M, 1 / 8)
     _check_close(_np(out), ref, "bf16", f"cross {kind}")
+
+
+def _wide_case(seed, B, M, H, d, L_lo, L_hi, std):
+    """Q and K ~ N(0, std^2), V ~ N(0, 1), bf16, ragged encoder lengths."""
+    g = torch.Generator().manual_seed(seed)
+    lens = torch.randint(L_lo, L_hi + 1, (B,), generator=g)
+    off = torch.cat([torch.zeros(1, dtype=torch.int64), lens.cumsum(0)]).to(torch.int32)
+    n = int(off[-1])
+    q = std * torch.randn((B * M, H, d), generator=g)
+    k = std * torch.randn((n, H, d), generator=g)
+    v = torch.randn((n, H, d), generator=g)
+    return tuple(x.to(torch.bfloat16) for x in (q, k, v)) + (off,)
+
+
+WIDE = [(d, std) for d in (32, 64, 128) for std in (2.0, 3.0)] + [(64, 4.0), (128, 4.0)]
+
+
+@pytest.mark.parametrize("d,std", WIDE, ids=[f"d{d}_std{s:g}" for d, s in WIDE])
+def test_cross_attn_wide_scores(gpu, d, std):
+    """Un-normalised activations: with Q/K spread 2-4 the scores span tens of
+    exp2 units, so any rounding of the scaled scores ahead of the softmax
+    shows up in the weights.  Ragged lengths (tails shorter than a key tile)
+    and a beam count off the tile; at spread 4 most rows also overflow the
+    fast pass and take the safe one."""
+    q, k, v, off = _wide_case(200 + d + int(10 * std), B=3, M=300, H=2, d=d, L_lo=1, L_hi=300,
+                              std=std)
+    M = 300
+    _log(f"[cross wide] d={d} std={std} L={np.diff(off.numpy()).tolist()}")
+    out = G.grace_cross_attn(q.to(gpu), k.to(gpu), v.to(gpu), off.to(gpu), M)
+    torch.cuda.synchronize()
+    ref = oracle.cross_attn(_np(q), _np(k), _np(v), off.numpy(), M, 1 / math.sqrt(d))
+    _check_close(_np(out), ref, "bf16", f"cross wide d={d} std={std}")
+
+
+@pytest.mark.parametrize("d", [32, 64, 128])
+def test_cross_attn_near_tied_large_scores(gpu, d):
+    """Scores of ~100-200 exp2 units (row sums far past 2^64: the safe pass)
+    that are nearly tied: every query is ~12 u and every key is u plus a large
+    component orthogonal to u (spread 8) plus a little noise along it, so the
+    scores differ only by fractions of a unit while the keys themselves differ
+    a lot.  A relative rounding of the scaled query of 2^-9 moves the scores by
+    several tenths of a unit here; the weights must not move."""
+    B, M, H, L = 2, 160, 2, 200
+    g = torch.Generator().manual_seed(300 + d)
+    u = torch.sign(torch.randn((B, 1, H, d), generator=g))
+    w = 8.0 * torch.randn((B, L, H, d), generator=g)
+    w = w - (w * u).sum(-1, keepdim=True) / d * u
+    q = (12 * u + 0.1 * torch.randn((B, M, H, d), generator=g)).reshape(B * M, H, d)
+    k = (u + w + 0.05 * torch.randn((B, L, H, d), generator=g)).reshape(B * L, H, d)
+    v = torch.randn((B * L, H, d), generator=g)
+    q, k, v = (x.to(torch.bfloat16) for x in (q, k, v))
+    off = torch.arange(0, B * L + 1, L, dtype=torch.int32)
+    _log(f"[cross near-tie] d={d}")
+    out = G.grace_cross_attn(q.to(gpu), k.to(gpu), v.to(gpu), off.to(gpu), M)
+    torch.cuda.synchronize()
+    ref, probs = oracle.cross_attn(_np(q), _np(k), _np(v), off.numpy(), M, 1 / math.sqrt(d),
+                                   return_probs=True)
+    # the case is what it claims: no key of a row holds most of the weight
+    top = max(float(np.median(p.max(axis=-1))) for p in probs)
+    _log(f"  median largest weight {top:.3f}")
+    assert top < 0.2
+    _check_close(_np(out), ref, "bf16", f"cross near-tie d={d}")
