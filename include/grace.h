@@ -41,7 +41,9 @@
  * Streams.  `stream` is a hipStream_t passed as void* (NULL = null stream).
  *   Work is enqueued on it and not waited for; the library does no host
  *   synchronisation and holds no global state besides the thread-local last
- *   HIP error, so calls from several threads on several streams are safe.
+ *   HIP error, so calls from several threads on several streams are safe
+ *   (grace_beam_step_noalloc, which keeps a scratch array per GPU, is the
+ *   one exception; see there).
  * Errors.  Every argument check runs on the host before any launch; a
  *   non-zero status means nothing was launched and nothing was written.  A
  *   HIP launch failure returns GRACE_ERR_HIP and grace_last_hip_error() gives
@@ -316,6 +318,34 @@ int32_t grace_beam_step(const void* logits, const float* prev_scores, const uint
                         int32_t B, int32_t M, int32_t V, int32_t k, int32_t dtype,
                         void* workspace, int64_t workspace_bytes, int32_t* parents,
                         int32_t* tokens, float* scores, void* stream);
+
+/* Largest workspace grace_beam_step_noalloc can serve: 80 MiB, enough for
+ * 64 requests x 4096 beams x 512 tokens (70.0 MiB). */
+#define GRACE_BEAM_STEP_NOALLOC_MAX_BYTES (80ll << 20)
+
+/*
+ * grace_beam_step for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same parents, tokens and scores, bit for bit, with no workspace
+ * argument.  The workspace is a scratch array inside the library, one per GPU,
+ * of GRACE_BEAM_STEP_NOALLOC_MAX_BYTES; it is set up on the first call on each
+ * GPU (with that GPU current) and held until the process ends.  No call
+ * allocates or frees device memory.
+ *
+ *   arguments   as for grace_beam_step, without workspace and workspace_bytes;
+ *               `stream` must belong to the current GPU
+ * Returns GRACE_ERR_SHAPE when grace_beam_step_workspace_bytes(B, M, V)
+ * exceeds GRACE_BEAM_STEP_NOALLOC_MAX_BYTES (nothing is launched), and the
+ * statuses of grace_beam_step otherwise.  All calls on one GPU share its
+ * scratch array: calls that overlap in time on one GPU (concurrent streams,
+ * other host threads) race and give unspecified results; calls ordered on one
+ * stream, or separated by synchronisation, do not.  The array's contents
+ * between calls are unspecified and never read before being written.
+ */
+int32_t grace_beam_step_noalloc(const void* logits, const float* prev_scores,
+                                const uint32_t* mask, int32_t B, int32_t M, int32_t V, int32_t k,
+                                int32_t dtype, int32_t* parents, int32_t* tokens, float* scores,
+                                void* stream);
 
 /*
  * The CD + GTM index (Sec. 4.4, App. A): the SID trie in CSR form.  Node 0 is

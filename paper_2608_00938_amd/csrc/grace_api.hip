@@ -1,8 +1,11 @@
 // C ABI of the decode-attention library: argument validation on the host,
-// dispatch to the gfx950 kernels, HIP error mapping.  Nothing here allocates,
-// synchronises or keeps state beyond the thread-local last HIP error.
+// dispatch to the gfx950 kernels, HIP error mapping.  Nothing here allocates
+// or synchronises; the only state is the thread-local last HIP error and the
+// per-GPU address of the allocation-free beam step's scratch array.
 #include <math.h>
 #include <stdint.h>
+
+#include <mutex>
 
 #include "../../include/grace.h"
 #include "kernels.hpp"
@@ -273,31 +276,108 @@ int64_t grace_beam_step_workspace_bytes(int32_t B, int32_t M, int32_t V) {
   return (int64_t)grace::beam_step_workspace_bytes(B, M, V);
 }
 
-int32_t grace_beam_step(const void* logits, const float* prev_scores, const uint32_t* mask,
-                        int32_t B, int32_t M, int32_t V, int32_t k, int32_t dtype,
-                        void* workspace, int64_t workspace_bytes, int32_t* parents,
-                        int32_t* tokens, float* scores, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Sizes of a beam step (shared by the workspace and the allocation-free entry
+// points); GRACE_OK, or the status to return, with B == 0 a no-op.
+int32_t check_beam_step_sizes(int32_t B, int32_t M, int32_t V, int32_t k, int32_t dtype) {
   if (dtype != GRACE_F32 && dtype != GRACE_BF16) return GRACE_ERR_UNSUPPORTED;
   if (B < 0 || M < 1 || V < 1 || (int64_t)B * M * V >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
   if (k < 1 || k > grace::beam_topk_max_k() || (int64_t)k > (int64_t)M * V) return GRACE_ERR_SHAPE;
   if ((int64_t)B * k >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
-  if (B == 0) return GRACE_OK;
+  return GRACE_OK;
+}
+
+// Pointers and overlaps of a beam step whose workspace is [workspace, +ws_bytes).
+int32_t check_beam_step_buffers(const void* logits, const float* prev_scores,
+                                const uint32_t* mask, int32_t B, int32_t M, int32_t V, int32_t k,
+                                int32_t dtype, const void* workspace, int64_t ws_bytes,
+                                const int32_t* parents, const int32_t* tokens,
+                                const float* scores) {
   if (!logits || !prev_scores || !parents || !tokens || !scores || !workspace) return GRACE_ERR_NULL;
-  const int64_t ws_need = (int64_t)grace::beam_step_workspace_bytes(B, M, V);
-  if (workspace_bytes < ws_need || ((uintptr_t)workspace & 7) != 0) return GRACE_ERR_SHAPE;
   const int64_t R = (int64_t)B * M, outb = (int64_t)B * k * 4;
   const Range ins[3] = {{logits, R * V * elem_bytes(dtype)}, {prev_scores, R * 4},
                         {mask, mask ? R * ((V + 31) / 32) * 4 : 0}};
-  const Range outs[4] = {{parents, outb}, {tokens, outb}, {scores, outb}, {workspace, ws_need}};
+  const Range outs[4] = {{parents, outb}, {tokens, outb}, {scores, outb}, {workspace, ws_bytes}};
   for (int i = 0; i < 4; ++i) {
     for (int j = i + 1; j < 4; ++j)
       if (overlaps(outs[i].p, outs[i].n, outs[j].p, outs[j].n)) return GRACE_ERR_ALIAS;
     for (const Range& r : ins)
       if (overlaps(outs[i].p, outs[i].n, r.p, r.n)) return GRACE_ERR_ALIAS;
   }
+  return GRACE_OK;
+}
+
+// Workspace of grace_beam_step_noalloc: one copy of this array per GPU, kept
+// until the process ends and shared by every call on that GPU.  Host code
+// reaches it only through the device address scratch_address() looks up.
+constexpr int64_t kNoAllocScratchBytes = GRACE_BEAM_STEP_NOALLOC_MAX_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current GPU's scratch array, looked up the first time
+// a call runs on that GPU (with it current) and kept for later calls.
+int32_t scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e);
+  if (dev < 0 || dev >= kMaxDevices) return GRACE_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e);
+    if (p == nullptr) return GRACE_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return GRACE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t grace_beam_step(const void* logits, const float* prev_scores, const uint32_t* mask,
+                        int32_t B, int32_t M, int32_t V, int32_t k, int32_t dtype,
+                        void* workspace, int64_t workspace_bytes, int32_t* parents,
+                        int32_t* tokens, float* scores, void* stream) {
+  int32_t st = check_beam_step_sizes(B, M, V, k, dtype);
+  if (st != GRACE_OK || B == 0) return st;
+  if (!logits || !prev_scores || !parents || !tokens || !scores || !workspace) return GRACE_ERR_NULL;
+  const int64_t ws_need = (int64_t)grace::beam_step_workspace_bytes(B, M, V);
+  if (workspace_bytes < ws_need || ((uintptr_t)workspace & 7) != 0) return GRACE_ERR_SHAPE;
+  st = check_beam_step_buffers(logits, prev_scores, mask, B, M, V, k, dtype, workspace, ws_need,
+                               parents, tokens, scores);
+  if (st != GRACE_OK) return st;
   return hip_status(grace::launch_beam_step(logits, prev_scores, mask, B, M, V, k,
                                             dtype == GRACE_BF16, workspace, parents, tokens,
                                             scores, (hipStream_t)stream));
+}
+
+int32_t grace_beam_step_noalloc(const void* logits, const float* prev_scores,
+                                const uint32_t* mask, int32_t B, int32_t M, int32_t V, int32_t k,
+                                int32_t dtype, int32_t* parents, int32_t* tokens, float* scores,
+                                void* stream) {
+  int32_t st = check_beam_step_sizes(B, M, V, k, dtype);
+  if (st != GRACE_OK || B == 0) return st;
+  const int64_t ws_need = (int64_t)grace::beam_step_workspace_bytes(B, M, V);
+  if (ws_need > kNoAllocScratchBytes) return GRACE_ERR_SHAPE;
+  if (!logits || !prev_scores || !parents || !tokens || !scores) return GRACE_ERR_NULL;
+  void* ws = nullptr;
+  st = scratch_address(&ws);
+  if (st != GRACE_OK) return st;
+  st = check_beam_step_buffers(logits, prev_scores, mask, B, M, V, k, dtype, ws, ws_need, parents,
+                               tokens, scores);
+  if (st != GRACE_OK) return st;
+  return hip_status(grace::launch_beam_step(logits, prev_scores, mask, B, M, V, k,
+                                            dtype == GRACE_BF16, ws, parents, tokens, scores,
+                                            (hipStream_t)stream));
 }
 
 }  // extern "C"

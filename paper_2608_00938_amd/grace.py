@@ -67,6 +67,8 @@ _SIGNATURES = {
     "grace_beam_step_workspace_bytes": [_c_int, _c_int, _c_int],
     "grace_beam_step": [_c_void_p, _c_void_p, _c_void_p, _c_int, _c_int, _c_int, _c_int, _c_int,
                         _c_void_p, ctypes.c_int64, _c_void_p, _c_void_p, _c_void_p, _c_void_p],
+    "grace_beam_step_noalloc": [_c_void_p, _c_void_p, _c_void_p, _c_int, _c_int, _c_int, _c_int,
+                                _c_int, _c_void_p, _c_void_p, _c_void_p, _c_void_p],
     "grace_gtm_mask": [ctypes.POINTER(GtmIndexC), ctypes.POINTER(GtmUserC), _c_void_p, _c_int,
                        _c_int, _c_void_p, _c_void_p, _c_void_p],
     "grace_trie_advance": [ctypes.POINTER(GtmIndexC), _c_void_p, _c_void_p, _c_void_p, _c_int,
@@ -295,6 +297,31 @@ def grace_beam_step(logits, prev_scores, B: int, M: int, k: int, mask=None, pare
                                    workspace.numel() * workspace.element_size(), _ptr(parents),
                                    _ptr(tokens), _ptr(scores), _stream(logits))
     _check(st, "grace_beam_step")
+    return parents, tokens, scores
+
+
+#: Largest workspace grace_beam_step_noalloc serves (GRACE_BEAM_STEP_NOALLOC_MAX_BYTES).
+BEAM_STEP_NOALLOC_MAX_BYTES = 80 << 20
+
+
+def grace_beam_step_noalloc(logits, prev_scores, B: int, M: int, k: int, mask=None, parents=None,
+                            tokens=None, scores=None):
+    """grace_beam_step without a workspace argument: the library's per-GPU
+    scratch array serves as the workspace, so the call allocates no device
+    memory when the outputs are given.  Calls that overlap in time on one GPU
+    race on that array."""
+    _contig(logits, prev_scores, mask, parents, tokens, scores)
+    dev = logits.device
+    if parents is None:
+        parents = torch.empty((B, k), dtype=torch.int32, device=dev)
+    if tokens is None:
+        tokens = torch.empty((B, k), dtype=torch.int32, device=dev)
+    if scores is None:
+        scores = torch.empty((B, k), dtype=torch.float32, device=dev)
+    st = library().grace_beam_step_noalloc(_ptr(logits), _ptr(prev_scores), _ptr(mask), B, M,
+                                           logits.shape[1], k, _dtype_code(logits), _ptr(parents),
+                                           _ptr(tokens), _ptr(scores), _stream(logits))
+    _check(st, "grace_beam_step_noalloc")
     return parents, tokens, scores
 
 

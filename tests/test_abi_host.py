@@ -260,6 +260,40 @@ def test_beam_step_rejects(kw, status):
     assert beam_step(**kw) == status
 
 
+def beam_step_noalloc(**kw):
+    a = dict(logits=ctypes.c_void_p(0x100000), prev=ctypes.c_void_p(0x180000), mask=None, B=2, M=8,
+             V=64, k=16, dtype=G.GRACE_BF16, par=ctypes.c_void_p(0x200000),
+             tok=ctypes.c_void_p(0x300000), sc=ctypes.c_void_p(0x400000), stream=None)
+    a.update(kw)
+    return G.library().grace_beam_step_noalloc(a["logits"], a["prev"], a["mask"], a["B"], a["M"],
+                                               a["V"], a["k"], a["dtype"], a["par"], a["tok"],
+                                               a["sc"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=7), G.GRACE_ERR_UNSUPPORTED),
+    (dict(k=0), G.GRACE_ERR_SHAPE), (dict(k=8 * 64 + 1), G.GRACE_ERR_SHAPE),
+    (dict(B=1 << 10, M=1 << 12, V=1 << 10, k=4), G.GRACE_ERR_SHAPE),   # B*M*V >= 2^31
+    (dict(B=128, M=4096, V=512, k=4096), G.GRACE_ERR_SHAPE),          # workspace > the scratch array
+    (dict(M=0), G.GRACE_ERR_SHAPE),
+    (dict(logits=None), G.GRACE_ERR_NULL), (dict(prev=None), G.GRACE_ERR_NULL),
+    (dict(par=None), G.GRACE_ERR_NULL), (dict(sc=None), G.GRACE_ERR_NULL),
+    (dict(B=0), G.GRACE_OK),
+])
+def test_beam_step_noalloc_rejects(kw, status):
+    assert beam_step_noalloc(**kw) == status
+
+
+def test_beam_step_noalloc_limit():
+    """The header's limit is the binding's, and it holds the 64 x 4096 x 512 step."""
+    text = open(HEADER).read()
+    m = re.search(r"#define GRACE_BEAM_STEP_NOALLOC_MAX_BYTES \((\d+)ll << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == G.BEAM_STEP_NOALLOC_MAX_BYTES
+    lib = G.library()
+    assert lib.grace_beam_step_workspace_bytes(64, 4096, 512) <= G.BEAM_STEP_NOALLOC_MAX_BYTES
+    assert lib.grace_beam_step_workspace_bytes(128, 4096, 512) > G.BEAM_STEP_NOALLOC_MAX_BYTES
+
+
 def test_beam_step_workspace_bytes():
     lib = G.library()
     assert lib.grace_beam_step_workspace_bytes(2, 0, 64) == -1
