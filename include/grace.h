@@ -275,7 +275,8 @@ int64_t grace_beam_topk_workspace_bytes(int32_t B, int32_t M, int32_t V);
  *   cand       device, fp32 [B*M, V]
  *   row_max    device, fp32 [B*M] or NULL: a speed hint (grace_beam_scores'
  *              row maxima); any values give the same result
- *   B, M, V    requests, beams per request, vocabulary; M*V below 2^31
+ *   B, M, V    requests, beams per request, vocabulary; M*V below 2^31 and
+ *              B*M*V below 2^40
  *   k          1 <= k <= min(M*V, grace_beam_topk_max_k())
  *   workspace  device, at least grace_beam_topk_workspace_bytes(B, M, V) bytes,
  *              8-byte aligned, caller-owned; contents on entry are ignored and

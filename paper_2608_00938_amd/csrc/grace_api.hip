@@ -36,9 +36,10 @@ int32_t check_shape(int32_t B, int32_t M, int32_t H, int32_t d, int32_t dtype, i
                     int64_t& row_bytes) {
   if (dtype != GRACE_F32 && dtype != GRACE_BF16) return GRACE_ERR_UNSUPPORTED;
   if (!supported_d(d)) return GRACE_ERR_UNSUPPORTED;
-  if (B < 0 || M < 0 || H < 1) return GRACE_ERR_SHAPE;
+  if (B < 0 || M < 0 || H < 1 || (int64_t)H * d >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
   R = (int64_t)B * M;
-  if (R * H * d >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
+  // each factor below 2^31 first, so that the product cannot overflow
+  if (R >= ((int64_t)1 << 31) || R * H * d >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
   row_bytes = (int64_t)H * d * elem_bytes(dtype);
   return GRACE_OK;
 }
@@ -253,6 +254,7 @@ int32_t grace_beam_topk(const float* cand, const float* row_max, int32_t B, int3
                         int32_t k, void* workspace, int64_t workspace_bytes, int32_t* parents,
                         int32_t* tokens, float* scores, void* stream) {
   if (B < 0 || M < 1 || V < 1 || (int64_t)M * V >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
+  if ((int64_t)B * M * V >= ((int64_t)1 << 40)) return GRACE_ERR_SHAPE;
   if (k < 1 || k > grace::beam_topk_max_k() || (int64_t)k > (int64_t)M * V) return GRACE_ERR_SHAPE;
   if ((int64_t)B * k >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
   if (B == 0) return GRACE_OK;
@@ -424,7 +426,7 @@ int32_t grace_gtm_mask(const grace_gtm_index* index, const grace_gtm_user* user,
     return GRACE_ERR_SHAPE;
   if (B < 0 || M < 0) return GRACE_ERR_SHAPE;
   const int64_t R = (int64_t)B * M, W = (index->vocab + 31) / 32;
-  if (R * W >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
+  if (R >= ((int64_t)1 << 31) || R * W >= ((int64_t)1 << 31)) return GRACE_ERR_SHAPE;
   if (R == 0) return GRACE_OK;
   if (!node_ids || !mask || !user->bitmask || !user->num_locations) return GRACE_ERR_NULL;
   if (user->max_locations > 0 && !user->bloom) return GRACE_ERR_NULL;

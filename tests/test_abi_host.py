@@ -85,6 +85,9 @@ def selfattn(**kw):
     (dict(out=None), G.GRACE_ERR_NULL), (dict(off=None), G.GRACE_ERR_NULL),
     (dict(k=None), G.GRACE_ERR_NULL), (dict(out=P2), G.GRACE_ERR_ALIAS),
     (dict(B=1 << 20, M=1 << 12, H=16), G.GRACE_ERR_SHAPE),
+    # sizes whose products do not fit 64 bits are rejected without overflowing
+    (dict(B=1 << 30, M=1 << 30, H=1 << 30), G.GRACE_ERR_SHAPE),
+    (dict(B=0, H=1 << 30, sum_L=1 << 30), G.GRACE_ERR_SHAPE),
     (dict(B=0), G.GRACE_OK), (dict(M=0, q=None, out=None), G.GRACE_OK),
 ])
 def test_cross_attn_rejects(kw, status):
@@ -218,6 +221,7 @@ def beam_topk(**kw):
     (dict(k=0), G.GRACE_ERR_SHAPE), (dict(k=8 * 64 + 1), G.GRACE_ERR_SHAPE),
     (dict(M=1 << 20, V=1 << 12, k=4), G.GRACE_ERR_SHAPE), (dict(M=0), G.GRACE_ERR_SHAPE),
     (dict(M=100, k=5000), G.GRACE_ERR_SHAPE),              # above grace_beam_topk_max_k
+    (dict(B=(1 << 31) - 1, M=1 << 15, V=(1 << 16) - 1, k=4), G.GRACE_ERR_SHAPE),   # B*M*V >= 2^40
     (dict(cand=None), G.GRACE_ERR_NULL), (dict(tok=None), G.GRACE_ERR_NULL),
     (dict(par=ctypes.c_void_p(0x300000 + 8)), G.GRACE_ERR_ALIAS),
     (dict(sc=ctypes.c_void_p(0x100000 + 40)), G.GRACE_ERR_ALIAS),
@@ -337,6 +341,7 @@ def _gtm_user(**kw):
     ({}, {}, dict(mask=None), G.GRACE_ERR_NULL),
     ({}, {}, dict(mask=ctypes.c_void_p(0x300000 + 2)), G.GRACE_ERR_ALIAS),   # over tokens
     ({}, {}, dict(mask=ctypes.c_void_p(0xB00000 - 8)), G.GRACE_ERR_ALIAS),   # over node ids
+    ({}, {}, dict(B=1 << 30, M=1 << 30), G.GRACE_ERR_SHAPE),
     ({}, {}, dict(B=0), G.GRACE_OK),
 ])
 def test_gtm_mask_rejects(ix, us, extra, status):
