@@ -88,10 +88,69 @@ def read_traffic():
         return None
 
 
+def host_cpu():
+    """Model name, logical CPUs and physical cores of this host (lscpu's fields
+    from /proc/cpuinfo), and the CPUs this process may run on."""
+    model, phys = "unknown", set()
+    cur = {}
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ":" in ln:
+                k, v = (x.strip() for x in ln.split(":", 1))
+                cur[k] = v
+                if k == "model name":
+                    model = v
+            elif cur:
+                phys.add((cur.get("physical id", "0"), cur.get("core id", cur.get("processor"))))
+                cur = {}
+        if cur:
+            phys.add((cur.get("physical id", "0"), cur.get("core id", cur.get("processor"))))
+    except OSError:
+        pass
+    return {"model": model, "logical_cpus": os.cpu_count(), "physical_cores": len(phys) or None,
+            "usable_cpus": len(os.sched_getaffinity(0))}
+
+
+def oracle_step_us(wl, inp, parents, t):
+    """One whole decode step of a small workload through the oracle: cross-attention
+    of every row, the table update and the self-attention of every row at step t."""
+    import oracle
+    scale = 1.0 / math.sqrt(wl.d)
+    ek, ev = (x.cpu() for x in inp.enc_kv)
+    qc, qs = inp.step_tensor("q_cross", t).cpu(), inp.step_tensor("q_self", t).cpu()
+    ks = [inp.step_tensor("k_new", j).cpu() for j in range(t + 1)]
+    vs = [inp.step_tensor("v_new", j).cpu() for j in range(t + 1)]
+    t0 = time.perf_counter()
+    oracle.cross_attn(qc, ek, ev, inp.offsets, wl.M, scale)
+    kp = np.zeros((t + 1, wl.R, wl.H, wl.d))
+    vp = np.zeros_like(kp)
+    table = None
+    for j in range(t + 1):
+        kp, vp, table = oracle.kv_append(kp, vp, table, parents[j], ks[j], vs[j], wl.B, wl.M, j)
+    oracle.self_attn_step(qs, kp, vp, table, t, scale)
+    return (time.perf_counter() - t0) * 1e6
+
+
+def cpu_baseline_small(dev):
+    """The oracle on one host thread for the three small workloads (one whole step
+    at the last step index each), next to their GPU step times."""
+    from threadpoolctl import threadpool_limits
+    from paper_2608_00938_amd import workloads as W
+    out = {}
+    with threadpool_limits(limits=1):
+        for name in ("tiny_fp32", "bf16_b8_m256", "bf16_b32_m1024"):
+            wl = W.WORKLOADS[name]
+            inp = W.DecodeInputs(wl, 0, dev)
+            parents = [inp.parents(t) for t in range(wl.steps)]
+            out[name] = round(oracle_step_us(wl, inp, parents, wl.steps - 1), 1)
+    return {"unit": "µs per decode step", "cores": 1, "kind": "oracle", "per_workload": out,
+            "sample": "one whole step (every row) at the last step index, one thread"}
+
+
 def cpu_baseline(wl, inp, parents, budget_s=12.0):
     """Time the fp64 oracle on host cores on a bounded sample of one step at t=T-1:
     whole requests (all beams and heads), added one at a time until the budget is
-    spent; scaled to the full step."""
+    spent; the per-request mean is extrapolated to the full step."""
     import oracle
     from threadpoolctl import threadpool_info
 
@@ -121,10 +180,11 @@ def cpu_baseline(wl, inp, parents, budget_s=12.0):
         nreq += 1
     per_step_us = elapsed / nreq * wl.B * 1e6
     return {"value": round(per_step_us, 1), "unit": "µs per decode step", "cores": int(threads),
-            "kind": "oracle",
+            "kind": "oracle", "extrapolated": nreq < wl.B, "host_cpu": host_cpu(),
             "sample": f"{nreq} of {wl.B} requests (all {wl.M} beams, {wl.H} heads), one step at "
-                      f"t={t}: cross-attention + table rows + self-attention, fp64 numpy; "
-                      f"{elapsed:.1f} s measured, scaled x{wl.B / nreq:.1f}"}
+                      f"t={t}: cross-attention + table rows + self-attention, fp64 numpy on "
+                      f"{threads} BLAS threads; {elapsed:.1f} s measured, extrapolated to the "
+                      f"full step (x{wl.B / nreq:.2f})"}
 
 
 def bench_beam_step(wl, dev, reps=10):
@@ -497,13 +557,22 @@ def main():
     app_ms, self_ms = float(np.mean(per["append"])), float(np.mean(per["self"]))
     fused_bytes = float(np.mean([fused_b[t] for t in t_used]))
 
+    def dist(ms):
+        """median and p90 of per-call times in µs"""
+        a = np.asarray(ms) * 1e3
+        return {"median": round(float(np.median(a)), 2), "p90": round(float(np.percentile(a, 90)), 2)}
+
     if fused:
         # the fused call is timed between events 1 and 2 (events 2 and 3 are back to back)
         fused_ms = float(np.mean(per["append"]))
         kernels_us = {"cross_attn": round(cross_ms * 1e3, 2),
                       "self_attn_step_fused": round(fused_ms * 1e3, 2),
                       "self_attn_fused_by_step": [round(float(np.mean(x)) * 1e3, 2)
-                                                  for x in per_t["append"]]}
+                                                  for x in per_t["append"]],
+                      "per_call": {"cross_attn": dist(per["cross"]),
+                                   "self_attn_step_fused": dist(per["append"]),
+                                   "self_attn_fused_by_step": [dist(x) for x in per_t["append"]],
+                                   "step": dist(step_ms)}}
         hbm = {"self_attn_fused_GBs": round(fused_bytes / (fused_ms * 1e-3) / 1e9, 1),
                "self_attn_fused_frac": round(fused_bytes / (fused_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
                "algorithmic_bytes_per_launch": round(fused_bytes),
@@ -511,6 +580,8 @@ def main():
     else:
         kernels_us = {"cross_attn": round(cross_ms * 1e3, 2), "kv_append": round(app_ms * 1e3, 2),
                       "self_attn_step": round(self_ms * 1e3, 2),
+                      "per_call": {"cross_attn": dist(per["cross"]), "kv_append": dist(per["append"]),
+                                   "self_attn_step": dist(per["self"]), "step": dist(step_ms)},
                       "kv_append_by_step": [round(float(np.mean(x)) * 1e3, 2) for x in per_t["append"]],
                       "self_attn_by_step": [round(float(np.mean(x)) * 1e3, 2) for x in per_t["self"]]}
         hbm = {"kv_append_GBs": round(app_bytes / (app_ms * 1e-3) / 1e9, 1),
@@ -570,6 +641,8 @@ def main():
     if not args.no_cpu_baseline:
         log("timing the oracle on host cores ...")
         result["cpu_baseline"] = cpu_baseline(wl, inp, parents_np)
+        if not args.no_extras:
+            result["cpu_baseline_small"] = cpu_baseline_small(dev)
     print(json.dumps(result, ensure_ascii=False), flush=True)
 
 
