@@ -62,6 +62,14 @@ def algorithmic(wl, sum_L, parents):
         table_b = R * 4 * (1 if t > 0 else 0) + R * t * 4 + R * (t + 1) * 4
         append_b.append(4 * slab + table_b)
         uniq = unique_ancestor_blocks(wl, parents, t)
+        if t == 0:
+            # one token: its weight is exactly 1, so out = its value; q and the
+            # key are not needed (attend: v read, out written; fused: k_new and
+            # v_new read, slab k/v and out written)
+            self_b.append(slab + E * s * uniq[0] + R * 4)
+            self_logical.append(2 * slab + R * 4)
+            fused_b.append(5 * slab + table_b)
+            continue
         self_b.append(2 * slab + sum(2 * E * s * u for u in uniq) + R * (t + 1) * 4)
         self_logical.append(2 * slab + 2 * (t + 1) * slab + R * (t + 1) * 4)
         # fused: q, k_new, v_new read, slab k/v and out written, ancestors j < t read once

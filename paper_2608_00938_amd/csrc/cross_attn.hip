@@ -177,8 +177,9 @@ __device__ __forceinline__ float max_with_other_half(float x) {
 //
 // Work split.  A workgroup is four waves (one per SIMD) of 32*kMB beams each,
 // and two workgroups share each CU, so every SIMD runs two independent waves.
-// XCD-aware workgroup ordering puts the beam tiles of one (request, head) on
-// one XCD, whose L2 then serves the request's K/V to all of them.
+// XCD-aware workgroup ordering (work_item) puts the beam tiles of one
+// (request, head) on one XCD, whose L2 then serves that head's K/V to all of
+// them, and gives every XCD the same share of each request.
 //
 // Software pipeline.  Each wave runs over 32-key steps so that its
 // instruction stream always holds independent matrix and vector work:
@@ -271,21 +272,46 @@ __device__ __forceinline__ void wait_vmem_upto(int n) {
   }
 }
 
+// Work item of workgroup i: (beam tile mt, request b, head h).  Workgroup i
+// runs on XCD x = i % 8.  When the head count is a multiple of 8, XCD x takes
+// the heads h = x (mod 8) of every request, so each XCD gets the same mix of
+// encoder lengths (the same work for ragged requests), and walks the requests
+// starting at request x*B/8, so that at any time the XCDs read different
+// requests' rows.  All beam tiles of one (request, head) run back to back on
+// one XCD, whose L2 then serves that head's K/V to all of them.
+__device__ __forceinline__ void work_item(uint32_t i, uint32_t n, int32_t n_mt, int32_t B,
+                                          int32_t H, int32_t& mt, int32_t& b, int32_t& h) {
+  constexpr uint32_t kXcds = 8;
+  if (H % kXcds != 0) {
+    const uint32_t tile = xcd_remap(i, n);
+    mt = (int32_t)(tile % (uint32_t)n_mt);
+    const uint32_t bh = tile / (uint32_t)n_mt;
+    h = (int32_t)(bh % (uint32_t)H);
+    b = (int32_t)(bh / (uint32_t)H);
+    return;
+  }
+  const uint32_t x = i % kXcds, k = i / kXcds;
+  const uint32_t hpx = (uint32_t)H / kXcds;            // heads per XCD and request
+  const uint32_t p = k / (uint32_t)n_mt;                // (request, head) pair of this XCD
+  mt = (int32_t)(k % (uint32_t)n_mt);
+  const uint32_t shift = x * (((uint32_t)B + kXcds - 1) / kXcds);
+  b = (int32_t)((p / hpx + shift) % (uint32_t)B);
+  h = (int32_t)((p % hpx) * kXcds + x);
+}
+
 template <int D>
 __global__ void __launch_bounds__(Cfg<D>::kThreads, 2)
 cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                             const uint16_t* __restrict__ v, const int32_t* __restrict__ off,
-                            uint16_t* __restrict__ out, int32_t M, int32_t H, int32_t sum_L,
-                            int32_t n_mt, float c) {
+                            uint16_t* __restrict__ out, int32_t B, int32_t M, int32_t H,
+                            int32_t sum_L, int32_t n_mt, float c) {
   using C = Cfg<D>;
   __shared__ __attribute__((aligned(16))) char lds[C::kLdsBytes];
   char* const kbuf0 = lds;                              // K ring: 4 tiles
   char* const vbuf0 = lds + C::kNBuf * C::kTileBytes;   // V ring: 4 tiles
 
-  const uint32_t tile = xcd_remap(blockIdx.x, gridDim.x);
-  const int32_t mt = tile % n_mt;
-  const int32_t bh = tile / n_mt;
-  const int32_t h = bh % H, b = bh / H;
+  int32_t mt, b, h;
+  work_item(blockIdx.x, gridDim.x, n_mt, B, H, mt, b, h);
   int32_t o0, L;
   request_span(off, b, sum_L, o0, L);
 
@@ -861,7 +887,7 @@ hipError_t launch_cross_attn(const void* q, const void* enc_k, const void* enc_v
     hipLaunchKernelGGL(cross_attn_bf16_kernel<DD>, dim3((unsigned)grid),                 \
                        dim3(Cfg<DD>::kThreads), 0, stream, (const uint16_t*)q,               \
                        (const uint16_t*)enc_k, (const uint16_t*)enc_v, enc_off, (uint16_t*)out, \
-                       M, H, sum_L, n_mt, c);                                                 \
+                       B, M, H, sum_L, n_mt, c);                                              \
     return hipGetLastError();                                                                 \
   }
     if (d == 32) GRACE_X(32)

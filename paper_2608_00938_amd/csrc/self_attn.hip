@@ -145,6 +145,13 @@ self_attn_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_pool,
   if (g >= total_chunks) return;   // wave-uniform when UNIFORM (rows are whole waves)
   const uint32_t r = row_of<UNIFORM>(g, per_row);
   const int32_t c = (int32_t)(g - r * (uint32_t)chunks_per_row);
+  if constexpr (NT == 1) {
+    // one token: its softmax weight is exactly 1, the output is its value
+    uint32_t id = (uint32_t)table[(int64_t)r * T_max];
+    id = id < nblocks ? id : nblocks - 1;
+    __builtin_nontemporal_store(v_pool[(int64_t)id * chunks_per_row + c], &out[g]);
+    return;
+  }
   u32x4 kc[NT], vc[NT];
   const u32x4 qc = __builtin_nontemporal_load(&q[g]);
 #pragma unroll
@@ -180,6 +187,16 @@ self_attn_fused_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_
 
   u32x4 kc[NT], vc[NT];
   int32_t ids[NT > 1 ? NT - 1 : 1];
+  if constexpr (STEP == 0) {
+    // step 0: one token, whose softmax weight is exactly 1, so the output is
+    // v_new; q is not needed, and k_new only for its copy into the slab
+    vc[0] = __builtin_nontemporal_load(&v_new[g]);
+    if (copy_k) __builtin_nontemporal_store(__builtin_nontemporal_load(&k_new[g]), &k_pool[g]);
+    if (copy_v) __builtin_nontemporal_store(vc[0], &v_pool[g]);
+    if (c == 0) table_next[(int64_t)r * T_max] = (int32_t)r;
+    __builtin_nontemporal_store(vc[0], &out[g]);
+    return;
+  }
   const u32x4 qc = __builtin_nontemporal_load(&q[g]);
   kc[STEP] = __builtin_nontemporal_load(&k_new[g]);
   vc[STEP] = __builtin_nontemporal_load(&v_new[g]);

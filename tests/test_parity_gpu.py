@@ -285,6 +285,11 @@ EDGE = [
     dict(dtype="f32", B=2, M=9, H=1, d=32, steps=8, L=1),
     dict(dtype="bf16", B=1, M=1, H=1, d=64, steps=8, L=1),
     dict(dtype="bf16", B=4, M=64, H=2, d=64, steps=4, L=64, parents="zipf", zipf_s=1.5),
+    # head counts that are multiples of 8 take the XCD-interleaved work order;
+    # request counts that are not multiples of 8 exercise its rotation
+    dict(dtype="bf16", B=3, M=70, H=8, d=64, steps=2, L_lo=5, L_hi=150),
+    dict(dtype="bf16", B=11, M=33, H=16, d=32, steps=2, L_lo=1, L_hi=90),
+    dict(dtype="bf16", B=9, M=200, H=8, d=128, steps=2, L_lo=30, L_hi=260),
 ]
 
 
