@@ -290,6 +290,10 @@ EDGE = [
     dict(dtype="bf16", B=3, M=70, H=8, d=64, steps=2, L_lo=5, L_hi=150),
     dict(dtype="bf16", B=11, M=33, H=16, d=32, steps=2, L_lo=1, L_hi=90),
     dict(dtype="bf16", B=9, M=200, H=8, d=128, steps=2, L_lo=30, L_hi=260),
+    # d = 64 with at least 512 beams takes the 512-beam (eight-wave) kernel:
+    # a second beam tile that is partly past M, ragged tails, single-tile requests
+    dict(dtype="bf16", B=3, M=700, H=8, d=64, steps=2, L_lo=1, L_hi=200),
+    dict(dtype="bf16", B=2, M=1536, H=2, d=64, steps=2, L_lo=60, L_hi=400, parents="zipf", zipf_s=1.1),
 ]
 
 
@@ -520,11 +524,12 @@ def _extreme_case(gpu, kind, B=3, M=96, H=2, d=64, L=200, seed=13):
     return q, k, v, off
 
 
-@pytest.mark.parametrize("kind", ["huge", "tiny"])
-def test_cross_attn_extreme_scores_take_the_safe_pass(gpu, kind):
+@pytest.mark.parametrize("kind,M", [("huge", 96), ("tiny", 96), ("huge", 520), ("tiny", 520)])
+def test_cross_attn_extreme_scores_take_the_safe_pass(gpu, kind, M):
     """Scores whose exp2 sums leave [2^-100, 2^64] fail the fast pass's check;
-    the workgroup's safe pass (exponent shift) still matches the fp64 oracle."""
-    q, k, v, off = _extreme_case(gpu, kind)
+    the workgroup's safe pass (exponent shift) still matches the fp64 oracle
+    (M = 520: the 512-beam kernel, with a second, mostly empty beam tile)."""
+    q, k, v, off = _extreme_case(gpu, kind, M=M)
     M = q.shape[0] // (off.numel() - 1)
     _log(f"[cross extreme] {kind}")
     out = G.grace_cross_attn(q.to(gpu), k.to(gpu), v.to(gpu), off.to(gpu), M)
@@ -545,36 +550,36 @@ def _wide_case(seed, B, M, H, d, L_lo, L_hi, std):
     return tuple(x.to(torch.bfloat16) for x in (q, k, v)) + (off,)
 
 
-WIDE = [(d, std) for d in (32, 64, 128) for std in (2.0, 3.0)] + [(64, 4.0), (128, 4.0)]
+WIDE = [(d, std, 300) for d in (32, 64, 128) for std in (2.0, 3.0)] + \
+    [(64, 4.0, 300), (128, 4.0, 300)] + [(64, std, 600) for std in (2.0, 3.0, 4.0)]
 
 
-@pytest.mark.parametrize("d,std", WIDE, ids=[f"d{d}_std{s:g}" for d, s in WIDE])
-def test_cross_attn_wide_scores(gpu, d, std):
+@pytest.mark.parametrize("d,std,M", WIDE, ids=[f"d{d}_std{s:g}_m{m}" for d, s, m in WIDE])
+def test_cross_attn_wide_scores(gpu, d, std, M):
     """Un-normalised activations: with Q/K spread 2-4 the scores span tens of
     exp2 units, so any rounding of the scaled scores ahead of the softmax
     shows up in the weights.  Ragged lengths (tails shorter than a key tile)
     and a beam count off the tile; at spread 4 most rows also overflow the
     fast pass and take the safe one."""
-    q, k, v, off = _wide_case(200 + d + int(10 * std), B=3, M=300, H=2, d=d, L_lo=1, L_hi=300,
+    q, k, v, off = _wide_case(200 + d + int(10 * std) + M, B=3, M=M, H=2, d=d, L_lo=1, L_hi=300,
                               std=std)
-    M = 300
-    _log(f"[cross wide] d={d} std={std} L={np.diff(off.numpy()).tolist()}")
+    _log(f"[cross wide] d={d} std={std} M={M} L={np.diff(off.numpy()).tolist()}")
     out = G.grace_cross_attn(q.to(gpu), k.to(gpu), v.to(gpu), off.to(gpu), M)
     torch.cuda.synchronize()
     ref = oracle.cross_attn(_np(q), _np(k), _np(v), off.numpy(), M, 1 / math.sqrt(d))
     _check_close(_np(out), ref, "bf16", f"cross wide d={d} std={std}")
 
 
-@pytest.mark.parametrize("d", [32, 64, 128])
-def test_cross_attn_near_tied_large_scores(gpu, d):
+@pytest.mark.parametrize("d,M", [(32, 160), (64, 160), (128, 160), (64, 600)])
+def test_cross_attn_near_tied_large_scores(gpu, d, M):
     """Scores of ~100-200 exp2 units (row sums far past 2^64: the safe pass)
     that are nearly tied: every query is ~12 u and every key is u plus a large
     component orthogonal to u (spread 8) plus a little noise along it, so the
     scores differ only by fractions of a unit while the keys themselves differ
     a lot.  A relative rounding of the scaled query of 2^-9 moves the scores by
     several tenths of a unit here; the weights must not move."""
-    B, M, H, L = 2, 160, 2, 200
-    g = torch.Generator().manual_seed(300 + d)
+    B, H, L = 2, 2, 200
+    g = torch.Generator().manual_seed(300 + d + M)
     u = torch.sign(torch.randn((B, 1, H, d), generator=g))
     w = 8.0 * torch.randn((B, L, H, d), generator=g)
     w = w - (w * u).sum(-1, keepdim=True) / d * u
@@ -583,7 +588,7 @@ def test_cross_attn_near_tied_large_scores(gpu, d):
     v = torch.randn((B * L, H, d), generator=g)
     q, k, v = (x.to(torch.bfloat16) for x in (q, k, v))
     off = torch.arange(0, B * L + 1, L, dtype=torch.int32)
-    _log(f"[cross near-tie] d={d}")
+    _log(f"[cross near-tie] d={d} M={M}")
     out = G.grace_cross_attn(q.to(gpu), k.to(gpu), v.to(gpu), off.to(gpu), M)
     torch.cuda.synchronize()
     ref, probs = oracle.cross_attn(_np(q), _np(k), _np(v), off.numpy(), M, 1 / math.sqrt(d),
