@@ -22,8 +22,8 @@
 // every global access instruction covers full rows instead of 16-byte pieces
 // of 32 rows.
 //
-// fp32 path (VALU, cross_attn_f32_kernel).  One lane per beam, K/V tiles in LDS
-// read as broadcasts, fp32 FMAs throughout.
+// fp32 path (VALU, cross_attn_f32_kernel).  d/32 lanes per beam, K/V tiles in
+// LDS read as broadcasts, fp32 FMAs throughout.
 #include <type_traits>
 
 #include "common.hpp"
@@ -41,7 +41,10 @@ __device__ __forceinline__ void request_span(const int32_t* off, int32_t b, int3
 }
 
 // ---------------------------------------------------------------------------
-// fp32 VALU kernel
+// fp32 VALU kernel.  G = d/32 consecutive lanes share a beam, each holding 32
+// dims of its query and output accumulator (at most 64 live values per lane
+// at any d); partial dot products meet in a DPP group sum.  K/V tiles sit in
+// LDS and are read as broadcasts across the beams of the workgroup.
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ void __launch_bounds__(64)
@@ -50,22 +53,26 @@ cross_attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k,
                       float* __restrict__ out, int32_t M, int32_t H, int32_t sum_L,
                       int32_t n_mt, float c) {
   constexpr int TILE = 32;
+  constexpr int G = D / 32;          // lanes per beam
+  constexpr int kBeams = 64 / G;     // beams per workgroup
   __shared__ float ks[TILE][D];
   __shared__ float vs[TILE][D];
   const uint32_t tile = xcd_remap(blockIdx.x, gridDim.x);
   const int32_t mt = tile % n_mt;
   const int32_t bh = tile / n_mt;
   const int32_t h = bh % H, b = bh / H;
-  const int32_t m = mt * 64 + threadIdx.x;
+  const int part = threadIdx.x % G;  // dims part*32 .. part*32+31
+  const int32_t m = mt * kBeams + threadIdx.x / G;
   int32_t o0, L;
   request_span(off, b, sum_L, o0, L);
   const int64_t E = (int64_t)H * D;
   const int64_t row = (int64_t)b * M + m;
+  const int64_t col = (int64_t)h * D + part * 32;
 
-  float qr[D], acc[D];
+  float qr[32], acc[32];
 #pragma unroll
-  for (int e = 0; e < D; ++e) {
-    qr[e] = m < M ? q[row * E + h * D + e] : 0.f;
+  for (int e = 0; e < 32; ++e) {
+    qr[e] = m < M ? q[row * E + col + e] : 0.f;
     acc[e] = 0.f;
   }
   float m_run = -INFINITY, l_run = 0.f;
@@ -73,10 +80,10 @@ cross_attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k,
     const int32_t n = min(TILE, L - t0);
     __syncthreads();
     for (int i = threadIdx.x; i < TILE * D; i += 64) {
-      const int key = i / D, col = i % D;
-      const int64_t src = (int64_t)(o0 + t0 + (key < n ? key : n - 1)) * E + h * D + col;
-      ks[key][col] = k[src];
-      vs[key][col] = v[src];
+      const int key = i / D, cc = i % D;
+      const int64_t src = (int64_t)(o0 + t0 + (key < n ? key : n - 1)) * E + h * D + cc;
+      ks[key][cc] = k[src];
+      vs[key][cc] = v[src];
     }
     __syncthreads();
     float s[TILE];
@@ -85,7 +92,8 @@ cross_attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k,
     for (int j = 0; j < TILE; ++j) {
       float a = 0.f;
 #pragma unroll
-      for (int e = 0; e < D; ++e) a = __builtin_fmaf(qr[e], ks[j][e], a);
+      for (int e = 0; e < 32; ++e) a = __builtin_fmaf(qr[e], ks[j][part * 32 + e], a);
+      a = group_sum<G>(a);
       s[j] = j < n ? a : -INFINITY;
       mx = fmaxf(mx, s[j]);
     }
@@ -94,19 +102,19 @@ cross_attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k,
     m_run = m_new;
     l_run *= alpha;
 #pragma unroll
-    for (int e = 0; e < D; ++e) acc[e] *= alpha;
+    for (int e = 0; e < 32; ++e) acc[e] *= alpha;
 #pragma unroll
     for (int j = 0; j < TILE; ++j) {
       const float p = fast_exp2((s[j] - m_new) * c);
       l_run += p;
 #pragma unroll
-      for (int e = 0; e < D; ++e) acc[e] = __builtin_fmaf(p, vs[j][e], acc[e]);
+      for (int e = 0; e < 32; ++e) acc[e] = __builtin_fmaf(p, vs[j][part * 32 + e], acc[e]);
     }
   }
   if (m < M) {
     const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;
 #pragma unroll
-    for (int e = 0; e < D; ++e) out[row * E + h * D + e] = acc[e] * inv;
+    for (int e = 0; e < 32; ++e) out[row * E + col + e] = acc[e] * inv;
   }
 }
 
@@ -897,7 +905,7 @@ hipError_t launch_cross_attn(const void* q, const void* enc_k, const void* enc_v
   } else {
 #define GRACE_X(DD)                                                                          \
   {                                                                                          \
-    const int32_t n_mt = (M + 63) / 64;                                                      \
+    const int32_t n_mt = (M + 64 / (DD / 32) - 1) / (64 / (DD / 32));                       \
     const int64_t grid = (int64_t)B * H * n_mt;                                             \
     hipLaunchKernelGGL(cross_attn_f32_kernel<DD>, dim3((unsigned)grid), dim3(64), 0, stream, \
                        (const float*)q, (const float*)enc_k, (const float*)enc_v, enc_off,   \

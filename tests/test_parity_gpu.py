@@ -598,3 +598,30 @@ def test_cross_attn_near_tied_large_scores(gpu, d, M):
     _log(f"  median largest weight {top:.3f}")
     assert top < 0.2
     _check_close(_np(out), ref, "bf16", f"cross near-tie d={d}")
+
+
+def test_decode_resumes_from_snapshot(gpu):
+    """The pools and block tables are caller-owned, so a decode can be
+    checkpointed: copying them after step 1 into a fresh cache and resuming
+    there gives bit-identical outputs and tables for the remaining steps."""
+    wl = W.custom(dtype="bf16", B=2, M=96, H=2, d=64, steps=5, L=40, parents="zipf", zipf_s=1.2)
+    ref = Decode(wl, 15, gpu, fused=True)
+    for t in range(wl.steps):
+        ref.run_step(t)
+    run = Decode(wl, 15, gpu, fused=True)
+    for t in range(2):
+        run.run_step(t)
+    torch.cuda.synchronize()
+    snap = [x.clone() for x in (run.cache.k_pool, run.cache.v_pool, *run.cache.tables)]
+    resumed = Decode(wl, 15, gpu, fused=True)
+    c = resumed.cache
+    for dst, src in zip((c.k_pool, c.v_pool, *c.tables), snap):
+        dst.copy_(src)
+    resumed.steps = list(run.steps)
+    for t in range(2, wl.steps):
+        got = resumed.run_step(t)
+        torch.cuda.synchronize()
+        want = ref.steps[t]
+        assert torch.equal(got["xs"], want["xs"]) and torch.equal(got["xc"], want["xc"]), t
+        assert torch.equal(got["table"][:, :t + 1], want["table"][:, :t + 1]), t
+    assert torch.equal(c.k_pool, ref.cache.k_pool) and torch.equal(c.v_pool, ref.cache.v_pool)

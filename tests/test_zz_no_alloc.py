@@ -62,3 +62,33 @@ def test_noalloc_rejects_oversized_step(gpu):
                                              base + (6 << 18), torch.cuda.current_stream().cuda_stream)
     assert st == G.GRACE_ERR_SHAPE
     assert int(buf.abs().sum()) == 0
+
+
+def test_noalloc_step_replays_in_a_graph(gpu):
+    """The no-alloc step recorded in a HIP graph (the callers it is for): every
+    replay, with other eager library work and host synchronisation in between,
+    gives the workspace entry point's outputs bit for bit."""
+    B, M, V, k = 4, 256, 512, 300
+    logits, prev, mask = _case(gpu, 60, B, M, V, k)
+    want = G.grace_beam_step(logits, prev, B, M, k, mask=mask)
+    p, t, s = _outs(gpu, B, k)
+    # one eager call first: the scratch array's address is looked up outside capture
+    G.grace_beam_step_noalloc(logits, prev, B, M, k, mask=mask, parents=p, tokens=t, scores=s)
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    assert torch.equal(p, want[0]) and torch.equal(t, want[1])
+    graph = G.capture(lambda: G.grace_beam_step_noalloc(logits, prev, B, M, k, mask=mask, parents=p,
+                                                        tokens=t, scores=s), stream)
+    other_logits, other_prev, _ = _case(gpu, 61, 2, 64, 100, 50, "f32")
+    for rep in range(3):
+        p.fill_(-7)
+        t.fill_(-7)
+        s.fill_(float("nan"))
+        G.grace_beam_step_noalloc(other_logits, other_prev, 2, 64, 50)   # overwrites the scratch array
+        torch.cuda.synchronize()
+        graph.launch(stream)
+        stream.synchronize()
+        assert torch.equal(p, want[0]) and torch.equal(t, want[1]), rep
+        assert torch.equal(s.view(torch.int32), want[2].view(torch.int32)), rep
+        _log(f"  graph replay {rep}: identical")
+    graph.destroy()
