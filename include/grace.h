@@ -456,6 +456,30 @@ int32_t grace_graph_launch(void* graph_exec, void* stream);
 int32_t grace_graph_destroy(void* graph_exec);
 int32_t grace_graph_last_hip_error(void);
 
+/* Number of counters grace_debug_counts fills. */
+#define GRACE_DEBUG_KINDS 8
+
+/*
+ * Device-side checks of the debug build.  The library also builds as
+ * libgrace_debug.so (sources compiled with -DGRACE_DEBUG): the same entry
+ * points and results, but the attention kernels (cross-attention, append,
+ * self-attention, fused) count every index they had to clamp and check each
+ * global row index they compute against the extent of its buffer.  This call
+ * synchronises the current GPU, copies the counters to counts[0 ..
+ * GRACE_DEBUG_KINDS-1] and clears them:
+ *   counts[0]  request offsets out of order or outside [0, sum_L]
+ *   counts[1]  parents outside [0, M_prev)
+ *   counts[2]  block ids outside the pool
+ *   counts[3]  computed row indices outside their buffer (an indexing error)
+ *   counts[4..7] unused (0)
+ * Each is a number of checking lanes or workgroups, not of distinct inputs.
+ *
+ *   counts   host uint32 [GRACE_DEBUG_KINDS], written (zeros on any error)
+ * Returns GRACE_OK in the debug build and GRACE_ERR_UNSUPPORTED in the
+ * release build (counts all zero); GRACE_ERR_NULL for a NULL counts.
+ */
+int32_t grace_debug_counts(uint32_t* counts);
+
 /* Human-readable name of a status code (static storage; never NULL). */
 const char* grace_status_string(int32_t status);
 

@@ -1,7 +1,8 @@
 """Build libgrace.so in-tree with hipcc for gfx950.
 
 Usage: ``python -m paper_2608_00938_amd.build`` (also called by the repo's
-``__graft_entry__.build()``).  Every HIP source is compiled on each call.
+``__graft_entry__.build()``).  Every HIP source is compiled on each call, once
+for libgrace.so and once with -DGRACE_DEBUG for libgrace_debug.so.
 """
 from __future__ import annotations
 
@@ -34,18 +35,31 @@ def _run(cmd):
     return err
 
 
+DEBUG_LIB = os.path.join(PKG, "libgrace_debug.so")
+DEBUG_OBJ = os.path.join(OBJ, "debug")
+
+
 def build(verbose: bool = False) -> str:
-    os.makedirs(OBJ, exist_ok=True)
-    objs = [os.path.join(OBJ, s.replace(".hip", ".o")) for s in SOURCES]
+    """Build libgrace.so and its debug twin libgrace_debug.so (-DGRACE_DEBUG:
+    device-side index checks counted, see grace_debug_counts); returns the
+    release library's path."""
+    os.makedirs(DEBUG_OBJ, exist_ok=True)
+    jobs = []
+    for out_dir, extra in ((OBJ, []), (DEBUG_OBJ, ["-DGRACE_DEBUG"])):
+        for src in SOURCES:
+            jobs.append((src, os.path.join(out_dir, src.replace(".hip", ".o")), extra))
 
-    def compile_one(i):
-        return _run([HIPCC, *CFLAGS, "-c", os.path.join(CSRC, SOURCES[i]), "-o", objs[i]])
+    def compile_one(job):
+        src, obj, extra = job
+        return _run([HIPCC, *CFLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj])
 
-    with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        logs = list(ex.map(compile_one, range(len(SOURCES))))
-    tmp = LIB + ".tmp"
-    logs.append(_run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]))
-    os.replace(tmp, LIB)
+    with ThreadPoolExecutor(max_workers=min(len(jobs), os.cpu_count() or 1)) as ex:
+        logs = list(ex.map(compile_one, jobs))
+    for lib, out_dir in ((LIB, OBJ), (DEBUG_LIB, DEBUG_OBJ)):
+        objs = [os.path.join(out_dir, s.replace(".hip", ".o")) for s in SOURCES]
+        tmp = lib + ".tmp"
+        logs.append(_run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]))
+        os.replace(tmp, lib)
     if verbose:
         for lg in logs:
             if lg.strip():

@@ -27,13 +27,17 @@
 #include <type_traits>
 
 #include "common.hpp"
+#include "debug.hpp"
 #include "kernels.hpp"
 
 namespace grace {
 
+GRACE_DEBUG_COUNTERS;
+
 __device__ __forceinline__ void request_span(const int32_t* off, int32_t b, int32_t sum_L,
                                              int32_t& o0, int32_t& L) {
   int32_t a = off[b], e = off[b + 1];
+  if (threadIdx.x == 0) GRACE_DCHECK(0 <= a && a <= e && e <= sum_L, kDbgOffsets);
   a = a < 0 ? 0 : (a > sum_L ? sum_L : a);
   e = e < a ? a : (e > sum_L ? sum_L : e);
   o0 = a;
@@ -82,6 +86,7 @@ cross_attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k,
     for (int i = threadIdx.x; i < TILE * D; i += 64) {
       const int key = i / D, cc = i % D;
       const int64_t src = (int64_t)(o0 + t0 + (key < n ? key : n - 1)) * E + h * D + cc;
+      GRACE_DCHECK(o0 + t0 + (key < n ? key : n - 1) < sum_L, kDbgRow);
       ks[key][cc] = k[src];
       vs[key][cc] = v[src];
     }
@@ -320,6 +325,8 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
 
   int32_t mt, b, h;
   work_item(blockIdx.x, gridDim.x, n_mt, B, H, mt, b, h);
+  if (threadIdx.x == 0)
+    GRACE_DCHECK(0 <= b && b < B && 0 <= h && h < H && 0 <= mt && mt < n_mt, kDbgRow);
   int32_t o0, L;
   request_span(off, b, sum_L, o0, L);
 
@@ -363,13 +370,17 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
     const uint32_t dst = lds_base + (t & (C::kNBuf - 1)) * C::kTileBytes;
     if (t0 + C::kTileN <= L) {
 #pragma unroll
-      for (int i = 0; i < C::kLoads; ++i) load_to_lds(base, dma_off[i], dst + i * C::kThreads * 16);
+      for (int i = 0; i < C::kLoads; ++i) {
+        GRACE_DCHECK(o0 + t0 + (i * C::kThreads + (int)threadIdx.x) / C::kCPR < sum_L, kDbgRow);
+        load_to_lds(base, dma_off[i], dst + i * C::kThreads * 16);
+      }
     } else {
 #pragma unroll
       for (int i = 0; i < C::kLoads; ++i) {
         const int key = (i * C::kThreads + (int)threadIdx.x) / C::kCPR;
         const int over = key - (L - 1 - t0);   // > 0: past the last token
         const uint32_t o = over > 0 ? dma_off[i] - (uint32_t)over * (uint32_t)E * 2u : dma_off[i];
+        GRACE_DCHECK(o0 + t0 + (over > 0 ? key - over : key) < sum_L, kDbgRow);
         load_to_lds(base, o, dst + i * C::kThreads * 16);
       }
     }
@@ -421,6 +432,7 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
       const int row = sl / C::kCPR;
       const int chunk = (sl % C::kCPR) ^ tile_swizzle<D>(row);
       const int r = row < last ? row : last;
+      GRACE_DCHECK(m_base + r < M, kDbgRow);
       load_to_lds<true>(qbase, (uint32_t)(r * E + chunk * 8) * 2u, q_lds + i * 1024);
     }
   }
@@ -877,9 +889,24 @@ cross_attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restric
       const int ch = ln % C::kCPR;
       const u32x4 u = *(const u32x4*)(obuf + C::out_slot(row, ch) * 16);
       const int32_t m = m_base + row;
+      GRACE_DCHECK(b * M + m < B * M || m >= M, kDbgRow);
       if (m < M) __builtin_nontemporal_store(u, (u32x4*)(out + (b * M + m) * E + h * D + ch * 8));
     }
   }
+}
+
+hipError_t debug_take_cross(uint32_t* acc) {
+#ifdef GRACE_DEBUG
+  uint32_t tmp[kDbgKinds] = {};
+  const uint32_t zero[kDbgKinds] = {};
+  hipError_t e = hipMemcpyFromSymbol(tmp, HIP_SYMBOL(g_grace_debug), sizeof(tmp));
+  if (e == hipSuccess) e = hipMemcpyToSymbol(HIP_SYMBOL(g_grace_debug), zero, sizeof(zero));
+  for (int i = 0; i < kDbgKinds; ++i) acc[i] += tmp[i];
+  return e;
+#else
+  (void)acc;
+  return hipErrorNotSupported;
+#endif
 }
 
 hipError_t launch_cross_attn(const void* q, const void* enc_k, const void* enc_v,

@@ -52,6 +52,19 @@ extern "C" {
 
 int32_t grace_abi_version(void) { return GRACE_ABI_VERSION; }
 
+int32_t grace_debug_counts(uint32_t* counts) {
+  if (!counts) return GRACE_ERR_NULL;
+  for (int i = 0; i < GRACE_DEBUG_KINDS; ++i) counts[i] = 0;
+#ifdef GRACE_DEBUG
+  hipError_t e = hipDeviceSynchronize();
+  if (e == hipSuccess) e = grace::debug_take_cross(counts);
+  if (e == hipSuccess) e = grace::debug_take_self(counts);
+  return hip_status(e);
+#else
+  return GRACE_ERR_UNSUPPORTED;
+#endif
+}
+
 int32_t grace_last_hip_error(void) { return g_last_hip_error; }
 
 const char* grace_status_string(int32_t status) {

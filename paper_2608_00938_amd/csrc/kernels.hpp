@@ -67,4 +67,10 @@ hipError_t launch_trie_advance(const grace_gtm_index& index, const int32_t* node
                                int32_t M_prev, int32_t k, int32_t* node_next, int32_t* err_flag,
                                hipStream_t stream);
 
+// Debug builds: add the device-check counters of the attention kernels' source
+// files to acc[0 .. 7] and clear them (synchronous); release builds return
+// hipErrorNotSupported.
+hipError_t debug_take_cross(uint32_t* acc);
+hipError_t debug_take_self(uint32_t* acc);
+
 }  // namespace grace

@@ -4,9 +4,12 @@
 // Both kernels are HBM-bound gathers/copies: 16-byte vector loads and stores,
 // every load of a row issued before any of its arithmetic, fp32 math, no LDS.
 #include "common.hpp"
+#include "debug.hpp"
 #include "kernels.hpp"
 
 namespace grace {
+
+GRACE_DEBUG_COUNTERS;
 
 // ---------------------------------------------------------------------------
 // kv_append: new block-table rows from the parents' rows, fresh block for the
@@ -36,6 +39,7 @@ kv_append_kernel(u32x4* __restrict__ k_slab, u32x4* __restrict__ v_slab,
     int64_t src = 0;
     if (step > 0) {
       int32_t p = parents[r];
+      GRACE_DCHECK(0 <= p && p < M, kDbgParent);
       if (p < 0 || p >= M) {
         if (err_flag) *err_flag = 1;
         p = p < 0 ? 0 : M - 1;
@@ -148,6 +152,7 @@ self_attn_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_pool,
   if constexpr (NT == 1) {
     // one token: its softmax weight is exactly 1, the output is its value
     uint32_t id = (uint32_t)table[(int64_t)r * T_max];
+    GRACE_DCHECK(id < nblocks, kDbgBlockId);
     id = id < nblocks ? id : nblocks - 1;
     __builtin_nontemporal_store(v_pool[(int64_t)id * chunks_per_row + c], &out[g]);
     return;
@@ -157,6 +162,7 @@ self_attn_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_pool,
 #pragma unroll
   for (int j = 0; j < NT; ++j) {
     uint32_t id = (uint32_t)table[(int64_t)r * T_max + j];
+    GRACE_DCHECK(id < nblocks, kDbgBlockId);
     id = id < nblocks ? id : nblocks - 1;
     const int64_t off = (int64_t)id * chunks_per_row + c;
     kc[j] = k_pool[off];
@@ -202,6 +208,7 @@ self_attn_fused_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_
   vc[STEP] = __builtin_nontemporal_load(&v_new[g]);
   if constexpr (STEP > 0) {
     int32_t p = parents[r];
+    GRACE_DCHECK(0 <= p && p < M_prev, kDbgParent);
     if (p < 0 || p >= M_prev) {
       if (err_flag) *err_flag = 1;
       p = p < 0 ? 0 : M_prev - 1;
@@ -212,6 +219,7 @@ self_attn_fused_kernel(const u32x4* __restrict__ q, const u32x4* __restrict__ k_
     for (int j = 0; j < STEP; ++j) {
       uint32_t id = (uint32_t)table_prev[src * T_max + j];
       ids[j] = (int32_t)id;
+      GRACE_DCHECK(id < nblocks, kDbgBlockId);
       id = id < nblocks ? id : nblocks - 1;
       const int64_t off = (int64_t)id * chunks_per_row + c;
       kc[j] = k_pool[off];
@@ -306,6 +314,20 @@ static hipError_t launch_self_any(const SelfArgs& a, int32_t d, int32_t step, bo
   }
 #undef GRACE_SELF
   return hipErrorInvalidValue;
+}
+
+hipError_t debug_take_self(uint32_t* acc) {
+#ifdef GRACE_DEBUG
+  uint32_t tmp[kDbgKinds] = {};
+  const uint32_t zero[kDbgKinds] = {};
+  hipError_t e = hipMemcpyFromSymbol(tmp, HIP_SYMBOL(g_grace_debug), sizeof(tmp));
+  if (e == hipSuccess) e = hipMemcpyToSymbol(HIP_SYMBOL(g_grace_debug), zero, sizeof(zero));
+  for (int i = 0; i < kDbgKinds; ++i) acc[i] += tmp[i];
+  return e;
+#else
+  (void)acc;
+  return hipErrorNotSupported;
+#endif
 }
 
 hipError_t launch_self_attn_step(const void* q, const void* k_pool, const void* v_pool,

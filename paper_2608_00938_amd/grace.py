@@ -78,6 +78,7 @@ _SIGNATURES = {
     "grace_graph_launch": [_c_void_p, _c_void_p],
     "grace_graph_destroy": [_c_void_p],
     "grace_graph_last_hip_error": [],
+    "grace_debug_counts": [_c_void_p],
     "grace_status_string": [_c_int],
     "grace_last_hip_error": [],
     "grace_abi_version": [],
@@ -93,21 +94,48 @@ class GraceError(RuntimeError):
         super().__init__(f"{where}: {msg} [status {status}]")
 
 
+_DEBUG_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgrace_debug.so")
+_debug_lib = None
+GRACE_DEBUG_KINDS = 8
+
+
+def _load(path: str) -> ctypes.CDLL:
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with "
+                           "`python -m paper_2608_00938_amd.build`")
+    lib = ctypes.CDLL(path)
+    for name, args in _SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = (ctypes.c_char_p if name == "grace_status_string" else
+                      ctypes.c_int64 if name.endswith("_bytes") else _c_int)
+    return lib
+
+
 def library() -> ctypes.CDLL:
     """The loaded libgrace.so; raises if it has not been built."""
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB_PATH):
-            raise RuntimeError(f"{_LIB_PATH} is missing: build it with "
-                               "`python -m paper_2608_00938_amd.build`")
-        lib = ctypes.CDLL(_LIB_PATH)
-        for name, args in _SIGNATURES.items():
-            fn = getattr(lib, name)
-            fn.argtypes = args
-            fn.restype = (ctypes.c_char_p if name == "grace_status_string" else
-                          ctypes.c_int64 if name.endswith("_bytes") else _c_int)
-        _lib = lib
+        _lib = _load(_LIB_PATH)
     return _lib
+
+
+def debug_library() -> ctypes.CDLL:
+    """libgrace_debug.so: the same entry points with the device-side index
+    checks of the debug build (read with grace_debug_counts)."""
+    global _debug_lib
+    if _debug_lib is None:
+        _debug_lib = _load(_DEBUG_LIB_PATH)
+    return _debug_lib
+
+
+def grace_debug_counts(lib=None) -> list:
+    """Synchronise and read (and clear) the debug build's device-check counters:
+    [offsets, parents, block ids, computed rows, 0, 0, 0, 0]."""
+    lib = debug_library() if lib is None else lib
+    buf = (ctypes.c_uint32 * GRACE_DEBUG_KINDS)()
+    _check(lib.grace_debug_counts(buf), "grace_debug_counts")
+    return list(buf)
 
 
 def _ptr(t):

@@ -36,6 +36,23 @@ def test_header_declares_the_boundary():
         assert n in names
 
 
+def test_debug_counts_in_the_release_build():
+    """The release build has no device-check counters: zeros and UNSUPPORTED."""
+    lib = G.library()
+    buf = (ctypes.c_uint32 * 8)(*range(1, 9))
+    assert lib.grace_debug_counts(buf) == G.GRACE_ERR_UNSUPPORTED
+    assert list(buf) == [0] * 8
+    assert lib.grace_debug_counts(None) == G.GRACE_ERR_NULL
+
+
+def test_debug_build_exports_the_same_symbols():
+    if not os.path.exists(G._DEBUG_LIB_PATH):
+        pytest.skip("debug build not present")
+    dbg = G.debug_library()
+    for name in declared_functions():
+        assert hasattr(dbg, name), name
+
+
 def test_library_exports_every_declared_symbol():
     lib = G.library()
     for name in declared_functions():
