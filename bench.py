@@ -557,7 +557,8 @@ def main():
         wl, inp.sum_L, parents_np)
     cross_ms = float(np.mean(per["cross"]))
     achieved = cross_flops / (cross_ms * 1e-3) / 1e12
-    traffic = read_traffic()
+    # the committed counter summary covers the default workload only
+    traffic = read_traffic() if wl.name == WORKLOAD else None
     # HBM rooflines of the two gather/copy kernels: algorithmic bytes over the mean duration
     t_used = [k % T for k in range(args.steps)]
     app_bytes = float(np.mean([append_b[t] for t in t_used]))
@@ -610,15 +611,16 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": wl.dtype,
         "data": "synthetic",
         "config": {"workload": wl.name, "requests": wl.B, "beams": wl.M, "encoder_len": wl.L,
                    "heads": wl.H, "head_dim": wl.d, "decode_steps": T,
                    "parents": f"zipf(s={wl.zipf_s}) over beams, per-(request,step) permutation",
                    "step": ("cross_attn + self_attn_step_fused (append + attend)" if fused else
                             "cross_attn + kv_append (copy into slab) + self_attn_step")
-                           + ", t = k mod 4"},
-        "roofline": {"bound": "mfma", "kernel": "grace_cross_attn (cross_attn_bf16_kernel<64>)",
+                           + f", t = k mod {T}"},
+        "roofline": {"bound": "mfma",
+                     "kernel": f"grace_cross_attn (cross_attn_{'bf16' if wl.dtype == 'bf16' else 'f32'}_kernel<{wl.d}>)",
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
                      "algorithmic_flops_per_launch": cross_flops,
