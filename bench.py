@@ -31,6 +31,12 @@ METRIC = "µs per decode step (cross+self attn) at 64 req×4096 beams; MFMA % an
 WORKLOAD = "bf16_b64_m4096"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+# Vector-ALU ceiling of the softmax numerator: every score takes one v_mul_f32
+# (the scale), one v_exp_f32 (transcendental, quarter rate) and half a
+# v_cvt_pk_bf16_f32, i.e. 1 + 4 + 0.5 = 5.5 full-rate issue slots of 4 cycles
+# per 64 scores on a SIMD; 256 CUs x 4 SIMDs at 2.4 GHz.
+VALU_SLOTS_PER_SCORE = 5.5
+PEAK_SCORES_G = 256 * 4 * 64 / (4 * VALU_SLOTS_PER_SCORE) * 2.4   # Gscore/s
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "cross_attn_bf16_b64_m4096_traffic.txt")
 CROSS_SRC = os.path.join(ROOT, "paper_2608_00938_amd", "csrc", "cross_attn.hip")
 
@@ -556,6 +562,7 @@ def main():
     cross_flops, cross_bytes, append_b, self_b, self_logical, fused_b = algorithmic(
         wl, inp.sum_L, parents_np)
     cross_ms = float(np.mean(per["cross"]))
+    cross_scores = float(wl.H) * wl.M * inp.sum_L   # one exp2 per (beam, key, head)
     achieved = cross_flops / (cross_ms * 1e-3) / 1e12
     # the committed counter summary covers the default workload only
     traffic = read_traffic() if wl.name == WORKLOAD else None
@@ -625,6 +632,11 @@ def main():
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
                      "algorithmic_flops_per_launch": cross_flops,
                      "algorithmic_bytes_per_launch": cross_bytes},
+        "valu_roofline": {"bound": "alu", "kernel": "the same cross-attention launch",
+                          "what": "softmax numerators (scale, exp2, pack to bf16) on the vector ALU",
+                          "achieved": round(cross_scores / (cross_ms * 1e-3) / 1e9, 1),
+                          "peak": round(PEAK_SCORES_G, 1), "unit": "Gscore/s",
+                          "frac": round(cross_scores / (cross_ms * 1e-3) / 1e9 / PEAK_SCORES_G, 4)},
         "kernels_us": kernels_us,
         "hbm": hbm,
         "event_step_ms_median": round(float(np.median(step_ms)), 4),
