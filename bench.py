@@ -31,12 +31,13 @@ METRIC = "µs per decode step (cross+self attn) at 64 req×4096 beams; MFMA % an
 WORKLOAD = "bf16_b64_m4096"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
-# Vector-ALU ceiling of the softmax numerator: every score takes one v_mul_f32
-# (the scale), one v_exp_f32 (transcendental, quarter rate) and half a
-# v_cvt_pk_bf16_f32, i.e. 1 + 4 + 0.5 = 5.5 full-rate issue slots of 4 cycles
-# per 64 scores on a SIMD; 256 CUs x 4 SIMDs at 2.4 GHz.
-VALU_SLOTS_PER_SCORE = 5.5
-PEAK_SCORES_G = 256 * 4 * 64 / (4 * VALU_SLOTS_PER_SCORE) * 2.4   # Gscore/s
+# Vector-ALU ceiling of the softmax numerators: every score takes one
+# v_mul_f32 (the scale), one v_exp_f32 and half a v_cvt_pk_bf16_f32.  In the
+# 4-cycle issue units that SQ_ACTIVE_INST_VALU counts (one per VALU
+# instruction, two per v_exp_f32) that is 1 + 2 + 0.5 = 3.5 units per 64 scores
+# on a SIMD; 256 CUs x 4 SIMDs at 2.4 GHz.
+VALU_UNITS_PER_SCORE = 3.5
+PEAK_SCORES_G = 256 * 4 * 64 / (4 * VALU_UNITS_PER_SCORE) * 2.4   # Gscore/s
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "cross_attn_bf16_b64_m4096_traffic.txt")
 CROSS_SRC = os.path.join(ROOT, "paper_2608_00938_amd", "csrc", "cross_attn.hip")
 

@@ -204,7 +204,7 @@ __device__ __forceinline__ float max_with_other_half(float x) {
 //            into step j+1)
 //
 // in a fixed issue order: every 32x32x16 product is followed by the VALU work
-// that fits under it (two exp2 at the quarter rate), so that one wave alone
+// that fits under it (two multiply + exp2 pairs), so that one wave alone
 // keeps both the matrix core and the VALU busy.  Q^T stays in registers as
 // the input bf16 values; the softmax scale (times log2 e) multiplies the fp32
 // scores just before exp2, so the only roundings ahead of the softmax are those

@@ -73,6 +73,6 @@ def test_algorithmic_counts_follow_the_definitions():
 
 
 def test_vector_alu_ceiling():
-    # 1 + 4 + 0.5 issue slots of 4 cycles per 64 scores, 1024 SIMDs at 2.4 GHz
-    cycles_per_64 = 4 * (1 + 4 + 0.5)
+    # 1 + 2 + 0.5 issue units of 4 cycles per 64 scores, 1024 SIMDs at 2.4 GHz
+    cycles_per_64 = 4 * (1 + 2 + 0.5)
     assert bench.PEAK_SCORES_G == pytest.approx(1024 * 64 / cycles_per_64 * 2.4)
