@@ -290,8 +290,8 @@ EDGE = [
     dict(dtype="bf16", B=3, M=70, H=8, d=64, steps=2, L_lo=5, L_hi=150),
     dict(dtype="bf16", B=11, M=33, H=16, d=32, steps=2, L_lo=1, L_hi=90),
     dict(dtype="bf16", B=9, M=200, H=8, d=128, steps=2, L_lo=30, L_hi=260),
-    # d = 64 with at least 512 beams takes the 512-beam (eight-wave) kernel:
-    # a second beam tile that is partly past M, ragged tails, single-tile requests
+    # d = 64 with more than 256 beams: several 256-beam tiles per (request, head),
+    # the last one partly past M, ragged tails, single-tile requests
     dict(dtype="bf16", B=3, M=700, H=8, d=64, steps=2, L_lo=1, L_hi=200),
     dict(dtype="bf16", B=2, M=1536, H=2, d=64, steps=2, L_lo=60, L_hi=400, parents="zipf", zipf_s=1.1),
 ]
@@ -528,7 +528,7 @@ def _extreme_case(gpu, kind, B=3, M=96, H=2, d=64, L=200, seed=13):
 def test_cross_attn_extreme_scores_take_the_safe_pass(gpu, kind, M):
     """Scores whose exp2 sums leave [2^-100, 2^64] fail the fast pass's check;
     the workgroup's safe pass (exponent shift) still matches the fp64 oracle
-    (M = 520: the 512-beam kernel, with a second, mostly empty beam tile)."""
+    (M = 520: three 256-beam tiles, the last one mostly past M)."""
     q, k, v, off = _extreme_case(gpu, kind, M=M)
     M = q.shape[0] // (off.numel() - 1)
     _log(f"[cross extreme] {kind}")
